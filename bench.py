@@ -1,0 +1,203 @@
+"""Benchmark of the recomputation DP on one MI355X.
+
+One step is one pass of the whole path over one synthetic graph: build the
+lower-set family (rc_build_family), fill the DP table and select t*
+(rc_solve), trace the schedule back and re-evaluate it (rc_reconstruct).
+The graph itself is handed over (rc_graph_create) before the timed
+region, so the inputs are resident in HBM when timing starts.
+
+Prints one JSON line.  `value` is DP relaxations per second of wall time
+per step; `roofline` rates the DP fill kernel against the int32 VALU peak
+of MI355X with the fill time taken from HIP events that the library
+records on the fill's stream; `cpu_baseline` times the CPU oracle on the
+same graph on this host.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+# MI355X: 256 CUs, 64 int32 lanes per CU per clock, 2.4 GHz peak engine clock.
+VALU_INT32_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
+OPS_PER_RELAXATION = 3          # compare with tau, add dm, min into the target
+FILL_SOURCES = ["paper_1905_11722_amd/csrc/fill.hip"]
+
+
+def fill_source_hash():
+    h = hashlib.sha256()
+    for rel in FILL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(workload):
+    """HBM traffic of the fill from committed rocprofv3 PMC runs, if they were
+    taken on the current fill source; else None."""
+    path = os.path.join(ROOT, "profiles", f"fill_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("fill_source_sha256_16") != fill_source_hash():
+        return None
+    return rec.get("bytes_per_solve")
+
+
+def run_step(rcdp, g, case):
+    fam = g.build_family(case.mode)
+    sol = fam.solve(case.B, case.objective)
+    sched = sol.reconstruct() if sol.feasible else None
+    fill_ms = sol.fill_ms()
+    info = fam.info
+    t_star = sol.t_star
+    sol.free()
+    fam.free()
+    return info, fill_ms, t_star, sched
+
+
+def time_case(rcdp, torch, case, steps, warmup):
+    g = rcdp.Graph.create(case.graph)
+    for _ in range(warmup):
+        run_step(rcdp, g, case)
+    torch.cuda.synchronize()
+    fills = []
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        info, fill_ms, t_star, sched = run_step(rcdp, g, case)
+        fills.append(fill_ms)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    g.free()
+    return {
+        "ms_per_step": (t1 - t0) * 1e3 / steps,
+        "fill_ms": sum(fills) / len(fills),
+        "fill_ms_min": min(fills),
+        "info": info,
+        "t_star": t_star,
+        "k": None if sched is None else int(len(sched.chain)),
+    }
+
+
+def cpu_baseline(case, relaxations):
+    from oracle import oracle
+    t0 = time.perf_counter()
+    r = oracle.solve(case.graph, case.mode, case.B, case.objective)
+    dt = time.perf_counter() - t0
+    return {
+        "value": relaxations / dt,
+        "unit": "relaxations/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"one full {case.objective.upper()} solve of {case.name} "
+                   f"(Algorithm 1 over all {r.num_sets} sets, t over 0..T(V)), "
+                   f"single thread, {dt:.1f} s; t*={r.t_star}"),
+        "seconds": dt,
+        "t_star": r.t_star,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="densenet121")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-graphs", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (--gpus {args.gpus} requested): the DP of one "
+              "graph does not shard across GPUs; independent solves would.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_1905_11722_amd import rcdp, workloads
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    rcdp.load_library()
+
+    case = workloads.case(args.workload)
+    main_res = time_case(rcdp, torch, case, args.steps, args.warmup)
+    info = main_res["info"]
+    W = info["relaxations"]
+    step_s = main_res["ms_per_step"] / 1e3
+    fill_s = main_res["fill_ms"] / 1e3
+    achieved = OPS_PER_RELAXATION * W / fill_s / 1e12
+
+    per_graph = {}
+    if not args.no_other_graphs:
+        for name in workloads.CASES:
+            if name == args.workload:
+                r = main_res
+            else:
+                r = time_case(rcdp, torch, workloads.case(name), max(3, args.steps // 4), 1)
+            per_graph[name] = {
+                "wall_ms": round(r["ms_per_step"], 4),
+                "fill_ms": round(r["fill_ms"], 4),
+                "relaxations": r["info"]["relaxations"],
+                "relax_per_s_fill": r["info"]["relaxations"] / (r["fill_ms"] / 1e3)
+                if r["fill_ms"] > 0 else None,
+                "t_star": r["t_star"],
+                "k": r["k"],
+            }
+
+    out = {
+        "metric": "DP cell relaxations/sec (whole step: family + fill + traceback)",
+        "value": W / step_s,
+        "unit": "relaxations/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": main_res["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic",
+        "config": {
+            "workload": case.name,
+            "description": case.note,
+            "nodes": info["n"],
+            "family": case.mode,
+            "B": case.B,
+            "objective": case.objective,
+            "sets": info["num_sets"],
+            "pairs": info["num_pairs"],
+            "levels": info["num_levels"],
+            "T_total": info["T_total"],
+            "table_cells": info["table_cells"],
+            "relaxations": W,
+            "t_star": main_res["t_star"],
+        },
+        "fill_ms": main_res["fill_ms"],
+        "fill_relax_per_s": W / fill_s,
+        "roofline": {
+            "bound": "alu",
+            "achieved": achieved,
+            "peak": VALU_INT32_PEAK_TOPS,
+            "unit": "TOP/s (int32 VALU)",
+            "frac": achieved / VALU_INT32_PEAK_TOPS,
+            "traffic": read_traffic(case.name),
+            "kernel": "k_fill_level (all launches of one solve)",
+            "ops_per_relaxation": OPS_PER_RELAXATION,
+        },
+        "per_graph": per_graph,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(case, W)
+        assert out["cpu_baseline"]["t_star"] == main_res["t_star"], "oracle and GPU disagree on t*"
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,188 @@
+/*
+ * rc.h -- C ABI of the MI355X solver for the General Recomputation Problem
+ * of Kusumoto et al., "A Graph Theoretic Framework of Recomputation
+ * Algorithms for Memory-Efficient Backpropagation" (NeurIPS 2019).
+ *
+ * Problem (Section 3, definition of the General Recomputation Problem):
+ * given the computation DAG G = (V, E) of a network with per-node forward
+ * time T_v > 0 and memory size M_v > 0 (Section 2), and a memory budget B,
+ * find an increasing chain of lower sets L_1 < ... < L_k = V whose
+ * canonical strategy has the least recomputation overhead (Eq. 1) among
+ * those whose peak memory (Eq. 2) is at most B, or report that none exists.
+ * The solver is the dynamic program of Section 4.2 / Appendix A (Algorithm
+ * 1) over either the family of all lower sets (Section 4.2) or the pruned
+ * family of ancestor sets (Section 4.3), with the time-centric (minimum
+ * overhead) or memory-centric (maximum overhead, Section 4.4) selection.
+ *
+ * Life cycle:  rc_graph_create -> rc_build_family -> rc_solve ->
+ * rc_reconstruct / rc_export_table -> rc_solution_free -> rc_family_free
+ * -> rc_graph_free.  A handle must outlive every handle made from it.
+ *
+ * Conventions shared by every entry point:
+ *  - Every pointer argument named *_host is host memory owned by the caller;
+ *    the library copies what it needs and keeps no caller pointer.
+ *  - Device memory comes from the caller's allocator (alloc/free_fn/user of
+ *    rc_graph_create), or from hipMalloc/hipFree when alloc is NULL.  Each
+ *    handle owns the device buffers it allocated and releases them in its
+ *    *_free call.
+ *  - stream is a hipStream_t (NULL: the default stream).  Device work is
+ *    enqueued on it; entry points that return results to the host
+ *    synchronise that stream before returning.
+ *  - A negative return is an error: out-parameters are left untouched and
+ *    no handle is created.  RC_INFEASIBLE is a result, not an error.
+ *    Nothing crosses the ABI as an exception.
+ *  - Handles are not thread-safe; distinct handles may be used from
+ *    distinct threads.
+ *  - Node ids 0..n-1 are the caller's.  They fix the order of sets of equal
+ *    size (ascending numeric value sum_{v in L} 2^v), and through it which of
+ *    several equally good predecessors the traceback follows (the smallest
+ *    family index, as with the strict update of Algorithm 1).
+ */
+#ifndef RC_H
+#define RC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct rc_graph_s* rc_graph;       /* validated DAG, device-resident */
+typedef struct rc_family_s* rc_family;     /* lower-set family + pair data  */
+typedef struct rc_solution_s* rc_solution; /* DP table of one budget        */
+
+/* Device allocator: returns device memory of at least `bytes` bytes aligned
+ * to 256 bytes, or NULL.  free_fn releases a pointer returned by alloc. */
+typedef void* (*rc_alloc_fn)(size_t bytes, void* user);
+typedef void (*rc_free_fn)(void* ptr, void* user);
+
+enum rc_mode { RC_FAMILY_EXACT = 0, RC_FAMILY_PRUNED = 1 };
+enum rc_objective { RC_TIME_CENTRIC = 0, RC_MEMORY_CENTRIC = 1 };
+
+enum rc_status {
+  RC_OK = 0,
+  RC_INFEASIBLE = 1,        /* no chain meets the budget (a result) */
+  RC_E_ARG = -1,            /* bad argument: NULL, out of range, bad CSR */
+  RC_E_CYCLE = -2,          /* G has a directed cycle or a self-loop */
+  RC_E_COST = -3,           /* some T_v or M_v is not positive */
+  RC_E_TOO_MANY_SETS = -4,  /* the family exceeds max_sets or 65535 */
+  RC_E_OVERFLOW = -5,       /* a value exceeds the table's integer widths */
+  RC_E_NOMEM = -6,          /* the allocator returned NULL */
+  RC_E_DEVICE = -7,         /* a HIP call failed or a kernel reported an error */
+  RC_E_STATE = -9           /* the handle is in the wrong state for the call */
+};
+
+/* Family statistics (rc_family_info).
+ *  relaxations: the DP's unit of work, sum over predecessor pairs (L, L')
+ *  of w_L = T(L \ boundary(L)) + 1, the cells of row L that can be finite.
+ *  table_cells: sum over the family of w_L. */
+typedef struct {
+  int32_t n;            /* nodes */
+  int32_t words;        /* 64-bit words per set bitmask, ceil(n / 64) */
+  int64_t num_sets;     /* family size, including the empty set and V */
+  int64_t num_pairs;    /* pairs L proper subset of L', both in the family */
+  int64_t num_levels;   /* distinct set sizes (the DP's sequential steps) */
+  int64_t table_cells;
+  int64_t relaxations;
+  int64_t T_total;      /* T(V) */
+  int64_t M_total;      /* M(V) */
+  int64_t max_row;      /* max_L w_L */
+} rc_family_info;
+
+/*
+ * rc_graph_create -- validate G and its costs (Section 2) and copy them to
+ * the device.
+ *  n: number of nodes (0 allowed: then V is empty and the only chain is empty).
+ *  row_ptr_host[n+1], col_idx_host[row_ptr[n]]: successor lists in CSR form;
+ *    an entry w in row v is the edge (v, w), v directly needed to compute w.
+ *    row_ptr[0] == 0 and non-decreasing.  Duplicate edges are ignored.
+ *  T_host[n], M_host[n]: forward time and memory size, each >= 1.
+ *  alloc/free_fn/user: device allocator used by this graph and by every
+ *    family and solution made from it (NULL alloc: hipMalloc).
+ * Errors: RC_E_ARG (NULL pointer, n < 0, n > 4096, index out of range,
+ * row_ptr not monotone), RC_E_CYCLE (cycle or self-loop), RC_E_COST
+ * (T_v or M_v < 1), RC_E_OVERFLOW (T(V) >= 2^31 - 1 or M(V) >= 2^31 / 4),
+ * RC_E_NOMEM, RC_E_DEVICE.
+ */
+int rc_graph_create(int32_t n, const int32_t* row_ptr_host, const int32_t* col_idx_host,
+                    const int32_t* T_host, const int32_t* M_host, rc_alloc_fn alloc,
+                    rc_free_fn free_fn, void* user, void* stream, rc_graph* out);
+void rc_graph_free(rc_graph g);
+
+/*
+ * rc_build_family -- build the lower-set family of Algorithm 1 on the
+ * device, with every per-set and per-pair quantity the DP needs.
+ *  mode RC_FAMILY_EXACT: all lower sets L (delta^-(L) in L, Section 2),
+ *    the family of the exact DP (Section 4.2).
+ *  mode RC_FAMILY_PRUNED: L^v = {w : v reachable from w} for every v
+ *    (Section 4.3), plus the empty set and V, which the DP starts from and
+ *    ends at.
+ *  Sets are ordered by ascending size, then ascending numeric value; index
+ *  0 is the empty set and index num_sets-1 is V.
+ *  max_sets: cap on the family size (at most 65535).
+ * The family does not depend on B: one family serves any number of solves.
+ * Errors: RC_E_ARG, RC_E_TOO_MANY_SETS, RC_E_OVERFLOW (table cells or pairs
+ * beyond 2^40), RC_E_NOMEM, RC_E_DEVICE.
+ */
+int rc_build_family(rc_graph g, int32_t mode, int64_t max_sets, void* stream, rc_family* out);
+int rc_family_stats(rc_family f, rc_family_info* info);
+/* Family members as bitmasks: bits_host[s * words + w] holds nodes
+ * 64w..64w+63 of set s (bit v % 64), s in family order. */
+int rc_family_sets(rc_family f, uint64_t* bits_host, void* stream);
+void rc_family_free(rc_family f);
+
+/*
+ * rc_solve -- fill the DP table opt[L, t] (Section 4.2: the least cache
+ * memory M(U_i) over chains ending at L with overhead t whose segments all
+ * fit B) and select t* (Algorithm 1's final step).
+ *  B >= 0: memory budget in the units of M.  Budgets above 2 M(V) give the
+ *    same table as B = 2 M(V), since no segment of Eq. 2 exceeds 2 M(V).
+ *  objective RC_TIME_CENTRIC: t* = min{t : opt[V, t] finite};
+ *    RC_MEMORY_CENTRIC: t* = max{t : opt[V, t] finite} (Section 4.4).
+ *  *t_opt, *m_opt: t* and opt[V, t*], or -1 and -1 when infeasible.
+ * Returns RC_OK or RC_INFEASIBLE (both create *out, whose table can be
+ * exported), or an error: RC_E_ARG, RC_E_OVERFLOW (min(B, 2 M(V)) > 65534),
+ * RC_E_NOMEM, RC_E_DEVICE.
+ */
+int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solution* out,
+             int64_t* t_opt, int64_t* m_opt);
+/* Milliseconds between HIP events recorded on the solve's stream just
+ * before the first and just after the last DP-fill kernel of the solve. */
+int rc_solution_fill_ms(rc_solution s, float* ms);
+
+/*
+ * rc_reconstruct -- trace optarg back from (V, t*) (Section 4.2) and
+ * re-evaluate the resulting canonical strategy from its definition.
+ *  *k: chain length; chain_host[num_sets] (first *k used): family indices of
+ *    L_1 .. L_k (L_k = V).
+ *  seg_host[n]: 0-based index i of the segment V_{i+1} holding each node.
+ *  cached_host[n]: 1 iff the node is in U_k = union of boundary(L_i).
+ *  *overhead: Eq. 1, T(V \ U_k) (equals t*).  *peak: max_i of Eq. 2 (at
+ *  most B).  *cache_mem: M(U_k) (equals opt[V, t*]).
+ * Any of the output pointers may be NULL.
+ * Returns RC_OK, RC_INFEASIBLE (nothing written), RC_E_ARG, RC_E_DEVICE.
+ */
+int rc_reconstruct(rc_solution s, void* stream, int32_t* k, int32_t* chain_host,
+                   int32_t* seg_host, uint8_t* cached_host, int64_t* overhead,
+                   int64_t* peak, int64_t* cache_mem);
+
+/*
+ * rc_export_table -- copy rows [first_set, first_set + num_sets) of the
+ * table to the host, over the whole range t = 0..T(V) of Algorithm 1:
+ * m_host[r * (T(V)+1) + t] = opt[L, t] (-1 when infinite) and
+ * arg_host[...] = family index of optarg[L, t] (-1 when none).  Either
+ * output may be NULL.  Returns RC_OK, RC_E_ARG, RC_E_NOMEM, RC_E_DEVICE.
+ */
+int rc_export_table(rc_solution s, int64_t first_set, int64_t num_sets, int64_t* m_host,
+                    int32_t* arg_host, void* stream);
+void rc_solution_free(rc_solution s);
+
+/* Static description of a status code. */
+const char* rc_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RC_H */

@@ -1,0 +1,533 @@
+// Graph encoding and lower-set family construction on the device.
+//
+// Sets of nodes are bitmasks of `words` 64-bit words (node v is bit v % 64
+// of word v / 64).  Per-set work runs one wavefront per set with lane w
+// holding word w (at most 64 words, i.e. 4096 nodes), so unions,
+// differences and subset tests are single VALU ops per lane and set sums
+// are lane-local popcount-style loops followed by a wave reduction.
+#include <hip/hip_runtime.h>
+
+#include "rc_internal.h"
+
+namespace rcdp {
+
+namespace {
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ int64_t wave_sum_i64(int64_t x) {
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, kWave);
+  return x;
+}
+
+__device__ __forceinline__ uint64_t bcast_u64(uint64_t x, int lane) {
+  return __shfl(x, lane, kWave);
+}
+
+// Sum of c[v] over the set bits of one word (nodes 64*word + bit).
+__device__ __forceinline__ int64_t word_cost(uint64_t bits, int word, const int32_t* c) {
+  int64_t s = 0;
+  while (bits) {
+    const int b = __builtin_ctzll(bits);
+    s += c[word * 64 + b];
+    bits &= bits - 1;
+  }
+  return s;
+}
+
+// ---------------------------------------------------------------- graph
+
+__global__ void k_zero_u64(uint64_t* p, int64_t count) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0;
+}
+
+// Edge (v, w): bit w in succ[v], bit v in pred[w] (Section 2's delta sets
+// of single nodes).  Duplicate edges OR the same bit.
+__global__ void k_graph_masks(int n, int words, const int32_t* row_ptr, const int32_t* col_idx,
+                              uint64_t* succ, uint64_t* pred) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= n) return;
+  for (int e = row_ptr[v]; e < row_ptr[v + 1]; e++) {
+    const int w = col_idx[e];
+    atomicOr((unsigned long long*)&succ[(int64_t)v * words + (w >> 6)], 1ull << (w & 63));
+    atomicOr((unsigned long long*)&pred[(int64_t)w * words + (v >> 6)], 1ull << (v & 63));
+  }
+}
+
+// ------------------------------------------------------------- ancestors
+
+// L^v = {w : v reachable from w} (Section 4.3) = {v} + union of L^p over the
+// predecessors p of v.  Nodes are visited depth by depth (longest path from
+// a source), so every predecessor is final before it is read.  One
+// workgroup; the closure lives in LDS when it fits.
+template <bool kLds>
+__global__ __launch_bounds__(1024) void k_ancestors(int n, int words, int num_depths,
+                                                    const int32_t* by_depth,
+                                                    const int32_t* depth_ptr,
+                                                    const int32_t* pred_ptr,
+                                                    const int32_t* pred_idx, uint64_t* anc_out) {
+  extern __shared__ uint64_t lds_anc[];
+  uint64_t* anc = kLds ? lds_anc : anc_out;
+  for (int d = 0; d < num_depths; d++) {
+    const int b = depth_ptr[d], e = depth_ptr[d + 1];
+    const int items = (e - b) * words;
+    for (int it = threadIdx.x; it < items; it += blockDim.x) {
+      const int v = by_depth[b + it / words];
+      const int w = it % words;
+      uint64_t x = (v >> 6) == w ? (1ull << (v & 63)) : 0ull;
+      for (int q = pred_ptr[v]; q < pred_ptr[v + 1]; q++) x |= anc[(int64_t)pred_idx[q] * words + w];
+      anc[(int64_t)v * words + w] = x;
+    }
+    __syncthreads();
+  }
+  if (kLds) {
+    for (int it = threadIdx.x; it < n * words; it += blockDim.x) anc_out[it] = anc[it];
+  }
+}
+
+// Candidates of the pruned family, set-major: [0] = empty set,
+// [1 + v] = L^v, [n + 1] = V.
+__global__ void k_pruned_candidates(int n, int words, const uint64_t* anc, uint64_t* cand) {
+  const int64_t total = (int64_t)(n + 2) * words;
+  for (int64_t it = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; it < total;
+       it += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t c = it / words;
+    const int w = (int)(it % words);
+    uint64_t x;
+    if (c == 0) {
+      x = 0;
+    } else if (c <= n) {
+      x = anc[(c - 1) * words + w];
+    } else {
+      const int lo = w * 64;
+      const int cnt = n - lo;
+      x = cnt >= 64 ? ~0ull : ((1ull << cnt) - 1);
+    }
+    cand[it] = x;
+  }
+}
+
+// ---------------------------------------------------- exact enumeration
+
+// One size level of reverse search over lower sets.  A lower set X != {}
+// has the canonical parent X \ {x}, x the largest node id of X with no
+// successor inside X (removing such an x keeps delta^-(X \ {x}) inside).
+// For every parent P of size s and node v with v not in P and
+// delta^-(v) inside P, the child X = P + {v} is kept iff v is X's
+// canonical element: every node of P with a larger id has a successor in X
+// (v itself has none: a successor of v inside P would put v in P).
+// Children are appended through an atomic counter; their order within the
+// level is fixed afterwards by the rank kernel.
+__global__ __launch_bounds__(256) void k_enum_level(int n, int words, int s, const uint64_t* succ,
+                                                    const uint64_t* pred, uint64_t* cand,
+                                                    int64_t cap, int32_t* lvl, DevStatus* st) {
+  const int64_t pb = lvl[s], pe = lvl[s + 1];
+  const int64_t items = (pe - pb) * n;
+  for (int64_t it = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; it < items;
+       it += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t p = pb + it / n;
+    const int v = (int)(it % n);
+    const uint64_t* P = cand + p * words;
+    const int vw = v >> 6;
+    const uint64_t vb = 1ull << (v & 63);
+    if (P[vw] & vb) continue;
+    bool ok = true;
+    for (int w = 0; w < words && ok; w++) ok = (pred[(int64_t)v * words + w] & ~P[w]) == 0;
+    if (!ok) continue;
+    // every x in P with x > v needs a successor in X = P + {v}
+    for (int w = words - 1; w >= vw && ok; w--) {
+      uint64_t bits = P[w];
+      if (w == vw) bits &= ~((vb << 1) - 1);  // ids > v only
+      while (bits && ok) {
+        const int x = w * 64 + __builtin_ctzll(bits);
+        bits &= bits - 1;
+        bool has = false;
+        for (int u = 0; u < words && !has; u++) {
+          uint64_t X = P[u] | (u == vw ? vb : 0ull);
+          has = (succ[(int64_t)x * words + u] & X) != 0;
+        }
+        ok = has;
+      }
+    }
+    if (!ok) continue;
+    const unsigned long long slot = atomicAdd((unsigned long long*)&st->count, 1ull);
+    if ((int64_t)slot >= cap) {
+      st->overflow = 1;
+      continue;
+    }
+    for (int w = 0; w < words; w++) cand[(int64_t)slot * words + w] = P[w] | (w == vw ? vb : 0ull);
+  }
+}
+
+__global__ void k_enum_start(int words, uint64_t* cand, int32_t* lvl, DevStatus* st) {
+  for (int w = threadIdx.x; w < words; w += blockDim.x) cand[w] = 0;  // the empty set
+  if (threadIdx.x == 0) {
+    st->count = 1;
+    st->overflow = 0;
+    lvl[0] = 0;
+    lvl[1] = 1;
+  }
+}
+
+// After level s: sets of size s + 1 occupy [lvl[s+1], count).
+__global__ void k_enum_close(int s, int64_t cap, int32_t* lvl, DevStatus* st) {
+  const int64_t c = st->count;
+  lvl[s + 2] = (int32_t)(c < cap ? c : cap);
+}
+
+// --------------------------------------------------------------- ranking
+
+// Numeric comparison of two sets stored set-major (most significant word
+// first): -1, 0, 1.
+__device__ __forceinline__ int cmp_value(const uint64_t* a, const uint64_t* b, int words) {
+  for (int w = words - 1; w >= 0; w--)
+    if (a[w] != b[w]) return a[w] < b[w] ? -1 : 1;
+  return 0;
+}
+
+__device__ __forceinline__ int popcnt_set(const uint64_t* a, int words) {
+  int c = 0;
+  for (int w = 0; w < words; w++) c += __popcll(a[w]);
+  return c;
+}
+
+// Canonical order: ascending size, then ascending numeric value.
+// Exact family: candidates are grouped by size level (reverse search
+// yields no duplicates) and ranked within their level.  Pruned family:
+// candidates are [0] the empty set, [1..n] the sets L^v (pairwise distinct),
+// [n+1] V; V is dropped when some L^v already equals V.  Output is
+// word-major: bits[w * fstride + index].
+__global__ __launch_bounds__(256) void k_rank(int words, int mode, int n, const uint64_t* cand,
+                                              const int32_t* lvl, uint64_t* bits, int64_t fstride,
+                                              DevStatus* st) {
+  const int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  const uint64_t* X;
+  int64_t rank;
+  if (mode == RC_FAMILY_EXACT) {
+    const int64_t total = lvl[n + 1];
+    if (x >= total) return;
+    X = cand + x * words;
+    const int s = popcnt_set(X, words);
+    rank = lvl[s];
+    for (int64_t y = lvl[s]; y < lvl[s + 1]; y++)
+      if (y != x && cmp_value(cand + y * words, X, words) < 0) rank++;
+    if (x == 0) st->count = st->overflow ? st->count : total;
+  } else {
+    const int64_t total = (int64_t)n + 2;
+    if (x >= total) return;
+    bool vdup = n == 0;                    // V is the empty set itself
+    for (int64_t y = 1; y <= n && !vdup; y++) vdup = popcnt_set(cand + y * words, words) == n;
+    if (vdup && x == n + 1) return;
+    const int64_t valid = vdup ? n + 1 : n + 2;
+    X = cand + x * words;
+    const int sx = popcnt_set(X, words);
+    rank = 0;
+    for (int64_t y = 0; y < valid; y++) {
+      if (y == x) continue;
+      const uint64_t* Y = cand + y * words;
+      const int sy = popcnt_set(Y, words);
+      if (sy < sx || (sy == sx && cmp_value(Y, X, words) < 0)) rank++;
+    }
+    if (x == 0) st->count = valid;
+  }
+  if (rank >= fstride) {
+    st->error = 1;
+    return;
+  }
+  for (int w = 0; w < words; w++) bits[(int64_t)w * fstride + rank] = X[w];
+}
+
+// ------------------------------------------------------- per-set values
+
+// Per set L (one wave, lane w = word w):
+//   boundary(L) = {v in L : some successor of v outside L}  (Section 2)
+//   T(L), M(L), T(boundary), M(boundary)
+//   A(L) = M(delta+(L) \ L) + M(delta-(delta+(L) \ L) \ L), the terms (iii)
+//   and (iv) of Eq. 2 for the set L' = L (for a lower set L the
+//   predecessors of delta+(L) inside L add nothing outside L)
+//   w_L = T(L \ boundary(L)) + 1, the cells of row L that can be finite.
+__global__ __launch_bounds__(256) void k_set_quantities(
+    int64_t F, int words, int64_t fstride, const uint64_t* bits, const uint64_t* succ,
+    const uint64_t* pred, const int32_t* T, const int32_t* M, uint64_t* bd, int32_t* size,
+    int32_t* Tsum, int32_t* Msum, int32_t* Tbd, int32_t* Mbd, int32_t* A, int32_t* w_out) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t s = blockIdx.x * (int64_t)(blockDim.x / kWave) + threadIdx.x / kWave;
+  if (s >= F) return;
+  const bool active = lane < words;
+  const uint64_t L = active ? bits[(int64_t)lane * fstride + s] : 0ull;
+  uint64_t out = 0, bdw = 0;
+  for (int ww = 0; ww < words; ww++) {
+    uint64_t Lw = bcast_u64(L, ww);
+    while (Lw) {
+      const int v = ww * 64 + __builtin_ctzll(Lw);
+      Lw &= Lw - 1;
+      const uint64_t sv = active ? succ[(int64_t)v * words + lane] : 0ull;
+      out |= sv;
+      const bool leaves = __any((sv & ~L) != 0);
+      if (leaves && lane == ww) bdw |= 1ull << (v & 63);
+    }
+  }
+  out &= ~L;
+  uint64_t in2 = 0;
+  for (int ww = 0; ww < words; ww++) {
+    uint64_t Ow = bcast_u64(out, ww);
+    while (Ow) {
+      const int v = ww * 64 + __builtin_ctzll(Ow);
+      Ow &= Ow - 1;
+      if (active) in2 |= pred[(int64_t)v * words + lane];
+    }
+  }
+  in2 &= ~L;
+  const int64_t tl = wave_sum_i64(active ? word_cost(L, lane, T) : 0);
+  const int64_t ml = wave_sum_i64(active ? word_cost(L, lane, M) : 0);
+  const int64_t tb = wave_sum_i64(active ? word_cost(bdw, lane, T) : 0);
+  const int64_t mb = wave_sum_i64(active ? word_cost(bdw, lane, M) : 0);
+  const int64_t ao = wave_sum_i64(active ? word_cost(out, lane, M) : 0);
+  const int64_t ai = wave_sum_i64(active ? word_cost(in2, lane, M) : 0);
+  const int sz = (int)wave_sum_i64(active ? __popcll(L) : 0);
+  if (active) bd[(int64_t)lane * fstride + s] = bdw;
+  if (lane == 0) {
+    size[s] = sz;
+    Tsum[s] = (int32_t)tl;
+    Msum[s] = (int32_t)ml;
+    Tbd[s] = (int32_t)tb;
+    Mbd[s] = (int32_t)mb;
+    A[s] = (int32_t)(ao + ai);
+    w_out[s] = (int32_t)(tl - tb + 1);
+  }
+}
+
+__global__ void k_row_widths(int64_t F, const int32_t* w, int64_t* padded) {
+  const int64_t s = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (s < F) padded[s] = ((int64_t)w[s] + kRowAlign - 1) / kRowAlign * kRowAlign;
+}
+
+// ------------------------------------------------------------------ pairs
+
+// Subset test of family members i and j (word-major storage).
+__device__ __forceinline__ bool is_subset(const uint64_t* bits, int64_t fstride, int words,
+                                          int64_t i, int64_t j) {
+  for (int w = 0; w < words; w++)
+    if (bits[(int64_t)w * fstride + i] & ~bits[(int64_t)w * fstride + j]) return false;
+  return true;
+}
+
+// Predecessors of target j: i < j with L_i a proper subset of L_j.  The
+// family is sorted by size, so every proper subset has a smaller index;
+// equal sizes are never proper subsets.
+__global__ __launch_bounds__(256) void k_pair_count(int64_t F, int words, int64_t fstride,
+                                                    const uint64_t* bits, const int32_t* size,
+                                                    int64_t* counts) {
+  const int64_t j = blockIdx.x;
+  __shared__ int64_t acc;
+  if (threadIdx.x == 0) acc = 0;
+  __syncthreads();
+  int64_t c = 0;
+  const int sj = size[j];
+  for (int64_t i = threadIdx.x; i < j; i += blockDim.x)
+    if (size[i] < sj && is_subset(bits, fstride, words, i, j)) c++;
+  atomicAdd((unsigned long long*)&acc, (unsigned long long)c);
+  __syncthreads();
+  if (threadIdx.x == 0) counts[j] = acc;
+}
+
+// Pair data of (L = L_i, L' = L_j), in ascending i for every target j:
+//   dt = T((L' \ L) \ bd(L')) = T(L' \ bd(L')) - T(L) + T(L & bd(L'))
+//   dm = M(bd(L') \ L)        = M(bd(L')) - M(L & bd(L'))
+//   c  = 2 M(L' \ L) + A(L')  = 2 (M(L') - M(L)) + A(L')
+// so that the step of Algorithm 1 from (L, t, m) is admitted iff
+// m + c <= B and then lands on (L', t + dt) with cache m + dm.  Only the
+// two sums over L & bd(L') depend on the pair; bd(L') is small.
+// walg[j] = sum over predecessors of w_i.
+__global__ __launch_bounds__(256) void k_pair_write(
+    int64_t F, int words, int64_t fstride, const uint64_t* bits, const uint64_t* bd,
+    const int32_t* size, const int32_t* Tsum, const int32_t* Msum, const int32_t* Tbd,
+    const int32_t* Mbd, const int32_t* A, const int32_t* w, const int32_t* T, const int32_t* M,
+    const int64_t* pred_ptr, int32_t* pidx, int32_t* pdt, int32_t* pdm, int32_t* pc,
+    int64_t* walg) {
+  const int64_t j = blockIdx.x;
+  __shared__ int64_t base;
+  __shared__ int64_t wsum;
+  __shared__ int32_t wave_cnt[4];
+  if (threadIdx.x == 0) {
+    base = pred_ptr[j];
+    wsum = 0;
+  }
+  __syncthreads();
+  const int sj = size[j];
+  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+  int64_t my_w = 0;
+  for (int64_t i0 = 0; i0 < j; i0 += blockDim.x) {
+    const int64_t i = i0 + threadIdx.x;
+    const bool is = i < j && size[i] < sj && is_subset(bits, fstride, words, i, j);
+    const uint64_t mask = __ballot(is);
+    const int before = __popcll(mask & ((1ull << lane) - 1));
+    if (lane == 0) wave_cnt[wv] = __popcll(mask);
+    __syncthreads();
+    int64_t off = base;
+    for (int q = 0; q < wv; q++) off += wave_cnt[q];
+    if (is) {
+      int64_t ti = 0, mi = 0;
+      for (int ww = 0; ww < words; ww++) {
+        const uint64_t x = bits[(int64_t)ww * fstride + i] & bd[(int64_t)ww * fstride + j];
+        ti += word_cost(x, ww, T);
+        mi += word_cost(x, ww, M);
+      }
+      const int64_t p = off + before;
+      pidx[p] = (int32_t)i;
+      pdt[p] = (int32_t)((int64_t)Tsum[j] - Tbd[j] - Tsum[i] + ti);
+      pdm[p] = (int32_t)((int64_t)Mbd[j] - mi);
+      pc[p] = (int32_t)(2 * ((int64_t)Msum[j] - Msum[i]) + A[j]);
+      my_w += w[i];
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int64_t tot = 0;
+      for (int q = 0; q < (int)(blockDim.x / kWave); q++) tot += wave_cnt[q];
+      base += tot;
+    }
+    __syncthreads();
+  }
+  atomicAdd((unsigned long long*)&wsum, (unsigned long long)my_w);
+  __syncthreads();
+  if (threadIdx.x == 0) walg[j] = wsum;
+}
+
+// ------------------------------------------------------------ scan / sum
+
+// Exclusive scan of in[0..count) into out[0..count]; one workgroup.
+__global__ __launch_bounds__(1024) void k_scan(const int64_t* in, int64_t* out, int64_t count) {
+  __shared__ int64_t buf[1024];
+  __shared__ int64_t carry;
+  if (threadIdx.x == 0) carry = 0;
+  __syncthreads();
+  for (int64_t b = 0; b < count; b += 1024) {
+    const int64_t i = b + threadIdx.x;
+    const int64_t x = i < count ? in[i] : 0;
+    buf[threadIdx.x] = x;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {
+      const int64_t y = threadIdx.x >= (unsigned)off ? buf[threadIdx.x - off] : 0;
+      __syncthreads();
+      buf[threadIdx.x] += y;
+      __syncthreads();
+    }
+    if (i < count) out[i] = carry + buf[threadIdx.x] - x;
+    __syncthreads();
+    if (threadIdx.x == 1023) carry += buf[1023];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[count] = carry;
+}
+
+__global__ __launch_bounds__(1024) void k_sum(const int64_t* in, int64_t count, int64_t* out) {
+  __shared__ int64_t acc;
+  if (threadIdx.x == 0) acc = 0;
+  __syncthreads();
+  int64_t s = 0;
+  for (int64_t i = threadIdx.x; i < count; i += blockDim.x) s += in[i];
+  atomicAdd((unsigned long long*)&acc, (unsigned long long)s);
+  __syncthreads();
+  if (threadIdx.x == 0) *out = acc;
+}
+
+}  // namespace
+
+// ============================================================== launchers
+
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t s) {
+  hipLaunchKernelGGL(k_zero_u64, dim3(1), dim3(256), 0, s, static_cast<uint64_t*>(p),
+                     (int64_t)(bytes / 8));
+  return hipGetLastError();
+}
+
+hipError_t launch_graph_masks(rc_graph g, const int32_t* d_row_ptr, const int32_t* d_col_idx,
+                              hipStream_t s) {
+  const int64_t cnt = (int64_t)g->n * g->words;
+  hipLaunchKernelGGL(k_zero_u64, dim3(64), dim3(256), 0, s, g->dSucc, cnt);
+  hipLaunchKernelGGL(k_zero_u64, dim3(64), dim3(256), 0, s, g->dPred, cnt);
+  hipLaunchKernelGGL(k_graph_masks, dim3((g->n + 255) / 256), dim3(256), 0, s, g->n, g->words,
+                     d_row_ptr, d_col_idx, g->dSucc, g->dPred);
+  return hipGetLastError();
+}
+
+hipError_t launch_ancestors(rc_graph g, uint64_t* anc, hipStream_t s) {
+  const size_t lds = sizeof(uint64_t) * (size_t)g->n * g->words;
+  if (lds <= 48 * 1024) {
+    hipLaunchKernelGGL(k_ancestors<true>, dim3(1), dim3(1024), lds, s, g->n, g->words,
+                       g->num_depths, g->dByDepth, g->dDepthPtr, g->dPredPtr, g->dPredIdx, anc);
+  } else {
+    hipLaunchKernelGGL(k_ancestors<false>, dim3(1), dim3(1024), 0, s, g->n, g->words,
+                       g->num_depths, g->dByDepth, g->dDepthPtr, g->dPredPtr, g->dPredIdx, anc);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_pruned_candidates(rc_graph g, const uint64_t* anc, uint64_t* cand,
+                                    hipStream_t s) {
+  hipLaunchKernelGGL(k_pruned_candidates, dim3(32), dim3(256), 0, s, g->n, g->words, anc, cand);
+  return hipGetLastError();
+}
+
+hipError_t launch_enum_exact(rc_graph g, uint64_t* cand, int64_t cap, int32_t* lvl,
+                             DevStatus* st, hipStream_t s) {
+  hipLaunchKernelGGL(k_enum_start, dim3(1), dim3(64), 0, s, g->words, cand, lvl, st);
+  for (int lev = 0; lev < g->n; lev++) {
+    hipLaunchKernelGGL(k_enum_level, dim3(512), dim3(256), 0, s, g->n, g->words, lev, g->dSucc,
+                       g->dPred, cand, cap, lvl, st);
+    hipLaunchKernelGGL(k_enum_close, dim3(1), dim3(1), 0, s, lev, cap, lvl, st);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_rank(rc_graph g, int32_t mode, const uint64_t* cand, int64_t ncand_max,
+                       const int32_t* lvl, uint64_t* bits, int64_t fstride, DevStatus* st,
+                       hipStream_t s) {
+  hipLaunchKernelGGL(k_rank, dim3((unsigned)((ncand_max + 255) / 256)), dim3(256), 0, s, g->words,
+                     mode, g->n, cand, lvl, bits, fstride, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_set_quantities(rc_family f, hipStream_t s) {
+  rc_graph g = f->g;
+  const int per_block = 256 / kWave;
+  hipLaunchKernelGGL(k_set_quantities, dim3((unsigned)((f->F + per_block - 1) / per_block)),
+                     dim3(256), 0, s, f->F, g->words, f->fstride, f->bits, g->dSucc, g->dPred,
+                     g->dT, g->dM, f->bd, f->size, f->Tsum, f->Msum, f->Tbd, f->Mbd, f->A, f->w);
+  return hipGetLastError();
+}
+
+hipError_t launch_row_widths(rc_family f, int64_t* padded, hipStream_t s) {
+  hipLaunchKernelGGL(k_row_widths, dim3((unsigned)((f->F + 255) / 256)), dim3(256), 0, s, f->F,
+                     f->w, padded);
+  return hipGetLastError();
+}
+
+hipError_t launch_pair_count(rc_family f, int64_t* counts, hipStream_t s) {
+  hipLaunchKernelGGL(k_pair_count, dim3((unsigned)f->F), dim3(256), 0, s, f->F, f->g->words,
+                     f->fstride, f->bits, f->size, counts);
+  return hipGetLastError();
+}
+
+hipError_t launch_scan(const int64_t* in, int64_t* out, int64_t count, int64_t, hipStream_t s) {
+  hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, in, out, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_pair_write(rc_family f, int64_t* walg_per_target, hipStream_t s) {
+  rc_graph g = f->g;
+  hipLaunchKernelGGL(k_pair_write, dim3((unsigned)f->F), dim3(256), 0, s, f->F, g->words,
+                     f->fstride, f->bits, f->bd, f->size, f->Tsum, f->Msum, f->Tbd, f->Mbd, f->A,
+                     f->w, g->dT, g->dM, f->pred_ptr, f->pidx, f->pdt, f->pdm, f->pc,
+                     walg_per_target);
+  return hipGetLastError();
+}
+
+hipError_t launch_sum(const int64_t* in, int64_t count, int64_t* out, hipStream_t s) {
+  hipLaunchKernelGGL(k_sum, dim3(1), dim3(1024), 0, s, in, count, out);
+  return hipGetLastError();
+}
+
+}  // namespace rcdp

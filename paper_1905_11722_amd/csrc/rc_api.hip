@@ -1,0 +1,500 @@
+// Host side of the C ABI declared in include/rc.h: argument validation,
+// device memory plumbing and kernel orchestration.  Every step of the
+// method itself runs in the kernels of graph.hip, family.hip and fill.hip.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "rc_internal.h"
+
+using namespace rcdp;
+
+#define RC_HIP(x)                              \
+  do {                                         \
+    if ((x) != hipSuccess) return RC_E_DEVICE; \
+  } while (0)
+
+namespace rcdp {
+
+void* Arena::get(size_t bytes) {
+  if (bytes == 0) bytes = 1;
+  bytes = (bytes + 255) & ~size_t(255);
+  void* p = nullptr;
+  if (alloc) {
+    p = alloc(bytes, user);
+  } else if (hipMalloc(&p, bytes) != hipSuccess) {
+    p = nullptr;
+  }
+  if (p) ptrs.push_back(p);
+  return p;
+}
+
+void Arena::release_all() {
+  for (void* p : ptrs) {
+    if (alloc) {
+      if (free_fn) free_fn(p, user);
+    } else {
+      (void)hipFree(p);
+    }
+  }
+  ptrs.clear();
+}
+
+}  // namespace rcdp
+
+static hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+template <class T>
+static int upload(Arena& a, const T* host, int64_t count, T** dev, hipStream_t s) {
+  *dev = a.get_n<T>(count);
+  if (!*dev) return RC_E_NOMEM;
+  if (count > 0)
+    RC_HIP(hipMemcpyAsync(*dev, host, sizeof(T) * (size_t)count, hipMemcpyHostToDevice, s));
+  return RC_OK;
+}
+
+extern "C" {
+
+const char* rc_status_str(int status) {
+  switch (status) {
+    case RC_OK: return "ok";
+    case RC_INFEASIBLE: return "infeasible: no chain of lower sets meets the budget";
+    case RC_E_ARG: return "invalid argument";
+    case RC_E_CYCLE: return "the graph has a directed cycle or a self-loop";
+    case RC_E_COST: return "a node cost is not positive";
+    case RC_E_TOO_MANY_SETS: return "the lower-set family exceeds max_sets";
+    case RC_E_OVERFLOW: return "a value exceeds the table's integer widths";
+    case RC_E_NOMEM: return "device allocation failed";
+    case RC_E_DEVICE: return "HIP runtime or kernel error";
+    case RC_E_STATE: return "handle in the wrong state";
+    default: return "unknown status";
+  }
+}
+
+// ------------------------------------------------------------------ graph
+
+int rc_graph_create(int32_t n, const int32_t* row_ptr, const int32_t* col_idx, const int32_t* T,
+                    const int32_t* M, rc_alloc_fn alloc, rc_free_fn free_fn, void* user,
+                    void* stream, rc_graph* out) {
+  if (!out || n < 0 || n > kMaxNodes) return RC_E_ARG;
+  if (n > 0 && (!row_ptr || !T || !M)) return RC_E_ARG;
+  if (alloc && !free_fn) return RC_E_ARG;
+  // -- validation of the CSR and costs (Section 2: T_v > 0, M_v > 0)
+  int64_t nnz = 0;
+  if (n > 0) {
+    if (row_ptr[0] != 0) return RC_E_ARG;
+    for (int v = 0; v < n; v++)
+      if (row_ptr[v + 1] < row_ptr[v]) return RC_E_ARG;
+    nnz = row_ptr[n];
+    if (nnz > 0 && !col_idx) return RC_E_ARG;
+    for (int64_t e = 0; e < nnz; e++)
+      if (col_idx[e] < 0 || col_idx[e] >= n) return RC_E_ARG;
+  }
+  int64_t Ttot = 0, Mtot = 0;
+  for (int v = 0; v < n; v++) {
+    if (T[v] < 1 || M[v] < 1) return RC_E_COST;
+    Ttot += T[v];
+    Mtot += M[v];
+  }
+  if (Ttot >= (int64_t)INT32_MAX - 1 || Mtot >= ((int64_t)1 << 29)) return RC_E_OVERFLOW;
+  // -- deduplicated predecessor lists and topological depth (Kahn by levels)
+  std::vector<std::vector<int32_t>> preds(n);
+  for (int v = 0; v < n; v++) {
+    for (int64_t e = row_ptr[v]; e < row_ptr[v + 1]; e++) {
+      int w = col_idx[e];
+      if (w == v) return RC_E_CYCLE;
+      preds[w].push_back(v);
+    }
+  }
+  for (auto& p : preds) {
+    std::sort(p.begin(), p.end());
+    p.erase(std::unique(p.begin(), p.end()), p.end());
+  }
+  std::vector<int32_t> indeg(n), depth(n, 0), order;
+  order.reserve(n);
+  std::vector<std::vector<int32_t>> succs(n);
+  for (int w = 0; w < n; w++)
+    for (int v : preds[w]) succs[v].push_back(w);
+  for (int v = 0; v < n; v++) {
+    indeg[v] = (int32_t)preds[v].size();
+    if (indeg[v] == 0) order.push_back(v);
+  }
+  for (size_t q = 0; q < order.size(); q++) {
+    int v = order[q];
+    for (int w : succs[v]) {
+      depth[w] = std::max(depth[w], depth[v] + 1);
+      if (--indeg[w] == 0) order.push_back(w);
+    }
+  }
+  if ((int)order.size() != n) return RC_E_CYCLE;
+  int32_t D = 0;
+  for (int v = 0; v < n; v++) D = std::max(D, depth[v] + 1);
+  std::vector<int32_t> by_depth(n), depth_ptr(D + 1, 0);
+  for (int v = 0; v < n; v++) depth_ptr[depth[v] + 1]++;
+  for (int d = 0; d < D; d++) depth_ptr[d + 1] += depth_ptr[d];
+  {
+    std::vector<int32_t> fill(depth_ptr.begin(), depth_ptr.end() - 1);
+    for (int v = 0; v < n; v++) by_depth[fill[depth[v]]++] = v;
+  }
+  std::vector<int32_t> pred_ptr(n + 1, 0), pred_idx;
+  for (int v = 0; v < n; v++) {
+    pred_ptr[v + 1] = pred_ptr[v] + (int32_t)preds[v].size();
+    pred_idx.insert(pred_idx.end(), preds[v].begin(), preds[v].end());
+  }
+
+  rc_graph g = new (std::nothrow) rc_graph_s();
+  if (!g) return RC_E_NOMEM;
+  g->n = n;
+  g->words = (n + 63) / 64;
+  g->T_total = Ttot;
+  g->M_total = Mtot;
+  g->arena.alloc = alloc;
+  g->arena.free_fn = free_fn;
+  g->arena.user = user;
+  g->num_depths = D;
+  hipStream_t s = as_stream(stream);
+  int st = RC_OK;
+  int32_t *d_row_ptr = nullptr, *d_col_idx = nullptr;
+  std::vector<int32_t> rp(row_ptr ? row_ptr : nullptr, row_ptr ? row_ptr + n + 1 : nullptr);
+  std::vector<int32_t> ci(col_idx ? col_idx : nullptr, col_idx ? col_idx + nnz : nullptr);
+  if (st == RC_OK) st = upload(g->arena, T, n, &g->dT, s);
+  if (st == RC_OK) st = upload(g->arena, M, n, &g->dM, s);
+  if (st == RC_OK) st = upload(g->arena, pred_ptr.data(), n + 1, &g->dPredPtr, s);
+  if (st == RC_OK) st = upload(g->arena, pred_idx.data(), (int64_t)pred_idx.size(), &g->dPredIdx, s);
+  if (st == RC_OK) st = upload(g->arena, by_depth.data(), n, &g->dByDepth, s);
+  if (st == RC_OK) st = upload(g->arena, depth_ptr.data(), D + 1, &g->dDepthPtr, s);
+  if (st == RC_OK) st = upload(g->arena, rp.data(), (int64_t)rp.size(), &d_row_ptr, s);
+  if (st == RC_OK) st = upload(g->arena, ci.data(), (int64_t)ci.size(), &d_col_idx, s);
+  if (st == RC_OK) {
+    g->dSucc = g->arena.get_n<uint64_t>((int64_t)n * g->words);
+    g->dPred = g->arena.get_n<uint64_t>((int64_t)n * g->words);
+    if (!g->dSucc || !g->dPred) st = RC_E_NOMEM;
+  }
+  if (st == RC_OK && n > 0 && launch_graph_masks(g, d_row_ptr, d_col_idx, s) != hipSuccess)
+    st = RC_E_DEVICE;
+  // the host vectors above must stay alive until the copies have completed
+  if (st == RC_OK && hipStreamSynchronize(s) != hipSuccess) st = RC_E_DEVICE;
+  if (st != RC_OK) {
+    (void)hipStreamSynchronize(s);
+    g->arena.release_all();
+    delete g;
+    return st;
+  }
+  *out = g;
+  return RC_OK;
+}
+
+void rc_graph_free(rc_graph g) {
+  if (!g) return;
+  (void)hipDeviceSynchronize();
+  g->arena.release_all();
+  delete g;
+}
+
+// ----------------------------------------------------------------- family
+
+static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
+  rc_graph g = f->g;
+  const int n = g->n, words = g->words;
+  Arena& A = f->arena;
+  Arena tmp;                       // scratch released at the end of the build
+  tmp.alloc = A.alloc;
+  tmp.free_fn = A.free_fn;
+  tmp.user = A.user;
+  struct TmpGuard {
+    Arena& a;
+    hipStream_t s;
+    ~TmpGuard() {
+      (void)hipStreamSynchronize(s);
+      a.release_all();
+    }
+  } guard{tmp, s};
+
+  f->status = A.get_n<DevStatus>(1);
+  if (!f->status) return RC_E_NOMEM;
+  RC_HIP(launch_zero(f->status, sizeof(DevStatus), s));
+
+  // ---- a2: the family as bitmasks, in canonical order
+  const int64_t cap = f->mode == RC_FAMILY_PRUNED ? (int64_t)n + 2 : max_sets;
+  f->fstride = cap;
+  uint64_t* cand = tmp.get_n<uint64_t>(cap * words);
+  int32_t* lvl = tmp.get_n<int32_t>(n + 3);
+  f->bits = A.get_n<uint64_t>(cap * words);
+  if (!cand || !lvl || !f->bits) return RC_E_NOMEM;
+  if (f->mode == RC_FAMILY_PRUNED) {
+    uint64_t* anc = tmp.get_n<uint64_t>((int64_t)n * words);
+    if (!anc) return RC_E_NOMEM;
+    if (n > 0) RC_HIP(launch_ancestors(g, anc, s));
+    RC_HIP(launch_pruned_candidates(g, anc, cand, s));
+  } else {
+    RC_HIP(launch_enum_exact(g, cand, cap, lvl, f->status, s));
+  }
+  RC_HIP(launch_rank(g, f->mode, cand, cap, lvl, f->bits, f->fstride, f->status, s));
+  DevStatus hs;
+  RC_HIP(hipMemcpyAsync(&hs, f->status, sizeof(hs), hipMemcpyDeviceToHost, s));
+  RC_HIP(hipStreamSynchronize(s));
+  if (hs.overflow) return RC_E_TOO_MANY_SETS;
+  if (hs.error) return RC_E_DEVICE;
+  const int64_t F = hs.count;
+  if (F < 1 || F > max_sets) return RC_E_TOO_MANY_SETS;
+  f->F = F;
+
+  // ---- a3: per-set quantities
+  f->size = A.get_n<int32_t>(F);
+  f->Tsum = A.get_n<int32_t>(F);
+  f->Msum = A.get_n<int32_t>(F);
+  f->Tbd = A.get_n<int32_t>(F);
+  f->Mbd = A.get_n<int32_t>(F);
+  f->A = A.get_n<int32_t>(F);
+  f->w = A.get_n<int32_t>(F);
+  f->bd = A.get_n<uint64_t>(f->fstride * words);
+  f->row_off = A.get_n<int64_t>(F + 1);
+  f->pred_ptr = A.get_n<int64_t>(F + 1);
+  int64_t* counts = tmp.get_n<int64_t>(F + 1);
+  int64_t* padded = tmp.get_n<int64_t>(F + 1);
+  int64_t* walg_t = tmp.get_n<int64_t>(F + 1);
+  if (!f->size || !f->Tsum || !f->Msum || !f->Tbd || !f->Mbd || !f->A || !f->w || !f->bd ||
+      !f->row_off || !f->pred_ptr || !counts || !padded || !walg_t)
+    return RC_E_NOMEM;
+  RC_HIP(launch_set_quantities(f, s));
+  // row offsets: rows padded to kRowAlign cells
+  RC_HIP(launch_row_widths(f, padded, s));
+  RC_HIP(launch_scan(padded, f->row_off, F, 1, s));
+
+  // ---- a4: predecessor pairs
+  RC_HIP(launch_pair_count(f, counts, s));
+  RC_HIP(launch_scan(counts, f->pred_ptr, F, 1, s));
+  int64_t P = 0;
+  RC_HIP(hipMemcpyAsync(&P, f->pred_ptr + F, sizeof(P), hipMemcpyDeviceToHost, s));
+  RC_HIP(hipStreamSynchronize(s));
+  if (P < 0 || P >= ((int64_t)1 << 40)) return RC_E_OVERFLOW;
+  f->P = P;
+  f->pidx = A.get_n<int32_t>(P);
+  f->pdt = A.get_n<int32_t>(P);
+  f->pdm = A.get_n<int32_t>(P);
+  f->pc = A.get_n<int32_t>(P);
+  if (!f->pidx || !f->pdt || !f->pdm || !f->pc) return RC_E_NOMEM;
+  RC_HIP(launch_pair_write(f, walg_t, s));
+  RC_HIP(launch_sum(walg_t, F, &f->status->walg, s));
+
+  // ---- host copies for launch configuration
+  std::vector<int32_t> size_h(F);
+  f->w_host.resize(F);
+  f->row_off_host.resize(F + 1);
+  RC_HIP(hipMemcpyAsync(size_h.data(), f->size, sizeof(int32_t) * F, hipMemcpyDeviceToHost, s));
+  RC_HIP(hipMemcpyAsync(f->w_host.data(), f->w, sizeof(int32_t) * F, hipMemcpyDeviceToHost, s));
+  RC_HIP(hipMemcpyAsync(f->row_off_host.data(), f->row_off, sizeof(int64_t) * (F + 1),
+                        hipMemcpyDeviceToHost, s));
+  RC_HIP(hipMemcpyAsync(&hs, f->status, sizeof(hs), hipMemcpyDeviceToHost, s));
+  RC_HIP(hipStreamSynchronize(s));
+  if (hs.error) return RC_E_DEVICE;
+  f->relax = hs.walg;
+  f->cells = f->row_off_host[F];
+  if (f->cells >= ((int64_t)1 << 40)) return RC_E_OVERFLOW;
+  f->level_ptr.clear();
+  f->level_maxw.clear();
+  f->max_row = 0;
+  for (int64_t i = 0; i < F; i++) {
+    if (i == 0 || size_h[i] != size_h[i - 1]) {
+      f->level_ptr.push_back(i);
+      f->level_maxw.push_back(0);
+    }
+    f->level_maxw.back() = std::max(f->level_maxw.back(), f->w_host[i]);
+    f->max_row = std::max<int64_t>(f->max_row, f->w_host[i]);
+  }
+  f->level_ptr.push_back(F);
+  return RC_OK;
+}
+
+int rc_build_family(rc_graph g, int32_t mode, int64_t max_sets, void* stream, rc_family* out) {
+  if (!g || !out) return RC_E_ARG;
+  if (mode != RC_FAMILY_EXACT && mode != RC_FAMILY_PRUNED) return RC_E_ARG;
+  if (max_sets < 1) return RC_E_ARG;
+  max_sets = std::min<int64_t>(max_sets, kMaxSets);
+  rc_family f = new (std::nothrow) rc_family_s();
+  if (!f) return RC_E_NOMEM;
+  f->g = g;
+  f->mode = mode;
+  f->arena.alloc = g->arena.alloc;
+  f->arena.free_fn = g->arena.free_fn;
+  f->arena.user = g->arena.user;
+  int st = build_family_impl(f, max_sets, as_stream(stream));
+  if (st != RC_OK) {
+    (void)hipStreamSynchronize(as_stream(stream));
+    f->arena.release_all();
+    delete f;
+    return st;
+  }
+  *out = f;
+  return RC_OK;
+}
+
+int rc_family_stats(rc_family f, rc_family_info* info) {
+  if (!f || !info) return RC_E_ARG;
+  info->n = f->g->n;
+  info->words = f->g->words;
+  info->num_sets = f->F;
+  info->num_pairs = f->P;
+  info->num_levels = (int64_t)f->level_ptr.size() - 1;
+  info->table_cells = 0;
+  for (int32_t x : f->w_host) info->table_cells += x;
+  info->relaxations = f->relax;
+  info->T_total = f->g->T_total;
+  info->M_total = f->g->M_total;
+  info->max_row = f->max_row;
+  return RC_OK;
+}
+
+int rc_family_sets(rc_family f, uint64_t* bits_host, void* stream) {
+  if (!f || !bits_host) return RC_E_ARG;
+  const int words = f->g->words;
+  hipStream_t s = as_stream(stream);
+  std::vector<uint64_t> wm((size_t)words * f->fstride);
+  if (!wm.empty())
+    RC_HIP(hipMemcpyAsync(wm.data(), f->bits, sizeof(uint64_t) * wm.size(), hipMemcpyDeviceToHost, s));
+  RC_HIP(hipStreamSynchronize(s));
+  for (int64_t i = 0; i < f->F; i++)
+    for (int w = 0; w < words; w++) bits_host[i * words + w] = wm[(size_t)w * f->fstride + i];
+  return RC_OK;
+}
+
+void rc_family_free(rc_family f) {
+  if (!f) return;
+  (void)hipDeviceSynchronize();
+  f->arena.release_all();
+  delete f;
+}
+
+// ------------------------------------------------------------------ solve
+
+int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solution* out,
+             int64_t* t_opt, int64_t* m_opt) {
+  if (!f || !out || B < 0) return RC_E_ARG;
+  if (objective != RC_TIME_CENTRIC && objective != RC_MEMORY_CENTRIC) return RC_E_ARG;
+  const int64_t Beff = std::min<int64_t>(B, 2 * f->g->M_total);
+  if (Beff > 0xFFFE) return RC_E_OVERFLOW;
+  hipStream_t s = as_stream(stream);
+  rc_solution sol = new (std::nothrow) rc_solution_s();
+  if (!sol) return RC_E_NOMEM;
+  sol->f = f;
+  sol->B = B;
+  sol->Beff = Beff;
+  sol->objective = objective;
+  sol->arena.alloc = f->arena.alloc;
+  sol->arena.free_fn = f->arena.free_fn;
+  sol->arena.user = f->arena.user;
+  auto fail = [&](int st) {
+    (void)hipStreamSynchronize(s);
+    if (sol->ev0) (void)hipEventDestroy(sol->ev0);
+    if (sol->ev1) (void)hipEventDestroy(sol->ev1);
+    sol->arena.release_all();
+    delete sol;
+    return st;
+  };
+  sol->m = sol->arena.get_n<uint16_t>(f->cells);
+  sol->arg = sol->arena.get_n<uint16_t>(f->cells);
+  sol->status = sol->arena.get_n<DevStatus>(1);
+  sol->chain = sol->arena.get_n<int32_t>(f->F);
+  sol->seg = sol->arena.get_n<int32_t>(f->g->n);
+  sol->cached = sol->arena.get_n<uint8_t>(f->g->n);
+  if (!sol->m || !sol->arg || !sol->status || !sol->chain || !sol->seg || !sol->cached)
+    return fail(RC_E_NOMEM);
+  if (hipEventCreate(&sol->ev0) != hipSuccess || hipEventCreate(&sol->ev1) != hipSuccess)
+    return fail(RC_E_DEVICE);
+  if (launch_solve_init(sol, s) != hipSuccess) return fail(RC_E_DEVICE);
+  if (hipEventRecord(sol->ev0, s) != hipSuccess) return fail(RC_E_DEVICE);
+  if (launch_fill(sol, s) != hipSuccess) return fail(RC_E_DEVICE);
+  if (hipEventRecord(sol->ev1, s) != hipSuccess) return fail(RC_E_DEVICE);
+  if (launch_select(sol, s) != hipSuccess) return fail(RC_E_DEVICE);
+  DevStatus hs;
+  if (hipMemcpyAsync(&hs, sol->status, sizeof(hs), hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return fail(RC_E_DEVICE);
+  if (hs.error) return fail(RC_E_DEVICE);
+  if (hipEventElapsedTime(&sol->fill_ms, sol->ev0, sol->ev1) != hipSuccess) sol->fill_ms = -1.f;
+  sol->t_star = hs.t_sel;
+  sol->m_star = hs.t_sel >= 0 ? hs.m_sel : -1;
+  sol->result = hs.t_sel >= 0 ? RC_OK : RC_INFEASIBLE;
+  if (t_opt) *t_opt = sol->t_star;
+  if (m_opt) *m_opt = sol->m_star;
+  *out = sol;
+  return sol->result;
+}
+
+int rc_solution_fill_ms(rc_solution s, float* ms) {
+  if (!s || !ms) return RC_E_ARG;
+  *ms = s->fill_ms;
+  return RC_OK;
+}
+
+int rc_reconstruct(rc_solution sol, void* stream, int32_t* k, int32_t* chain_host,
+                   int32_t* seg_host, uint8_t* cached_host, int64_t* overhead, int64_t* peak,
+                   int64_t* cache_mem) {
+  if (!sol) return RC_E_ARG;
+  if (sol->result != RC_OK) return RC_INFEASIBLE;
+  hipStream_t s = as_stream(stream);
+  rc_family f = sol->f;
+  const int n = f->g->n;
+  RC_HIP(launch_trace(sol, s));
+  DevStatus hs;
+  RC_HIP(hipMemcpyAsync(&hs, sol->status, sizeof(hs), hipMemcpyDeviceToHost, s));
+  std::vector<int32_t> ch(f->F), sg(n);
+  std::vector<uint8_t> ca(n);
+  RC_HIP(hipMemcpyAsync(ch.data(), sol->chain, sizeof(int32_t) * f->F, hipMemcpyDeviceToHost, s));
+  if (n > 0) {
+    RC_HIP(hipMemcpyAsync(sg.data(), sol->seg, sizeof(int32_t) * n, hipMemcpyDeviceToHost, s));
+    RC_HIP(hipMemcpyAsync(ca.data(), sol->cached, n, hipMemcpyDeviceToHost, s));
+  }
+  RC_HIP(hipStreamSynchronize(s));
+  if (hs.error || hs.k < 0 || hs.k > f->F) return RC_E_DEVICE;
+  if (k) *k = hs.k;
+  if (chain_host) std::copy(ch.begin(), ch.begin() + hs.k, chain_host);
+  if (seg_host) std::copy(sg.begin(), sg.end(), seg_host);
+  if (cached_host) std::copy(ca.begin(), ca.end(), cached_host);
+  if (overhead) *overhead = hs.overhead;
+  if (peak) *peak = hs.peak;
+  if (cache_mem) *cache_mem = hs.cache_mem;
+  return RC_OK;
+}
+
+int rc_export_table(rc_solution sol, int64_t first, int64_t count, int64_t* m_host,
+                    int32_t* arg_host, void* stream) {
+  if (!sol || first < 0 || count < 0 || first + count > sol->f->F) return RC_E_ARG;
+  rc_family f = sol->f;
+  hipStream_t s = as_stream(stream);
+  const int64_t W = f->g->T_total + 1;
+  const int64_t c0 = f->row_off_host[first], c1 = f->row_off_host[first + count];
+  std::vector<uint16_t> mm(c1 - c0), aa(c1 - c0);
+  if (c1 > c0) {
+    RC_HIP(hipMemcpyAsync(mm.data(), sol->m + c0, 2 * (c1 - c0), hipMemcpyDeviceToHost, s));
+    RC_HIP(hipMemcpyAsync(aa.data(), sol->arg + c0, 2 * (c1 - c0), hipMemcpyDeviceToHost, s));
+  }
+  RC_HIP(hipStreamSynchronize(s));
+  for (int64_t r = 0; r < count; r++) {
+    const int64_t set = first + r;
+    const int64_t off = f->row_off_host[set] - c0;
+    const int64_t w = f->w_host[set];
+    for (int64_t t = 0; t < W; t++) {
+      const bool in = t < w;
+      const uint32_t mv = in ? mm[off + t] : kInfM;
+      const uint32_t av = in ? aa[off + t] : kNoArg;
+      if (m_host) m_host[r * W + t] = mv == kInfM ? -1 : (int64_t)mv;
+      if (arg_host) arg_host[r * W + t] = (mv == kInfM || av == kNoArg) ? -1 : (int32_t)av;
+    }
+  }
+  return RC_OK;
+}
+
+void rc_solution_free(rc_solution sol) {
+  if (!sol) return;
+  (void)hipDeviceSynchronize();
+  if (sol->ev0) (void)hipEventDestroy(sol->ev0);
+  if (sol->ev1) (void)hipEventDestroy(sol->ev1);
+  sol->arena.release_all();
+  delete sol;
+}
+
+}  // extern "C"

@@ -1,0 +1,139 @@
+// Internal declarations of the MI355X recomputation-DP library.
+// Every kernel and launcher shared between the .hip translation units is
+// declared here; the C ABI lives in include/rc.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <vector>
+
+#include "rc.h"
+
+namespace rcdp {
+
+constexpr int kMaxNodes = 4096;                 // words <= 64 = one lane per word
+constexpr int kMaxWords = kMaxNodes / 64;
+constexpr int kMaxSets = 65535;                 // family index fits 16 bits
+constexpr uint32_t kInfM = 0xFFFFu;             // opt = infinity in a 16-bit cell
+constexpr uint32_t kNoArg = 0xFFFFu;            // optarg = none
+constexpr int64_t kRowAlign = 64;               // cells; rows start on 128-byte lines
+
+// Device allocator with ownership tracking.
+struct Arena {
+  rc_alloc_fn alloc = nullptr;
+  rc_free_fn free_fn = nullptr;
+  void* user = nullptr;
+  std::vector<void*> ptrs;
+  void* get(size_t bytes);                     // nullptr on failure
+  template <class T> T* get_n(int64_t count) {
+    return static_cast<T*>(get(sizeof(T) * (size_t)(count > 0 ? count : 1)));
+  }
+  void release_all();
+};
+
+// Small device status block: error flags and scalar results.
+struct DevStatus {
+  int32_t error;         // nonzero: a kernel found an inconsistency
+  int32_t overflow;      // family enumeration exceeded its cap
+  int64_t count;         // enumeration counter / family size
+  int32_t t_sel;         // selection result
+  int32_t m_sel;
+  int64_t walg;          // relaxations
+  int32_t k;             // chain length
+  int32_t pad0;
+  int64_t overhead, peak, cache_mem;
+};
+
+}  // namespace rcdp
+
+struct rc_graph_s {
+  int32_t n = 0, words = 0;
+  int64_t T_total = 0, M_total = 0;
+  rcdp::Arena arena;
+  // device
+  int32_t* dT = nullptr;          // [n]
+  int32_t* dM = nullptr;          // [n]
+  uint64_t* dSucc = nullptr;      // [n][words] successor masks
+  uint64_t* dPred = nullptr;      // [n][words] predecessor masks
+  int32_t* dPredPtr = nullptr;    // [n+1] predecessor CSR
+  int32_t* dPredIdx = nullptr;
+  int32_t* dByDepth = nullptr;    // nodes sorted by depth (longest path from a source)
+  int32_t* dDepthPtr = nullptr;   // [num_depths+1]
+  int32_t num_depths = 0;
+};
+
+struct rc_family_s {
+  rc_graph g = nullptr;
+  int32_t mode = 0;
+  int64_t F = 0, P = 0, cells = 0, relax = 0, max_row = 0;
+  int64_t fstride = 0;            // stride of the word-major bitmask arrays
+  rcdp::Arena arena;
+  // device: family, word-major [words][fstride]
+  uint64_t* bits = nullptr;
+  uint64_t* bd = nullptr;
+  // device: per set [F]
+  int32_t *size = nullptr, *Tsum = nullptr, *Msum = nullptr, *Tbd = nullptr, *Mbd = nullptr;
+  int32_t *A = nullptr, *w = nullptr;
+  int64_t* row_off = nullptr;     // [F+1], rows padded to kRowAlign cells
+  // device: predecessor pairs, CSR by target
+  int64_t* pred_ptr = nullptr;    // [F+1]
+  int32_t *pidx = nullptr, *pdt = nullptr, *pdm = nullptr, *pc = nullptr;
+  rcdp::DevStatus* status = nullptr;
+  // host copies used for launches
+  std::vector<int64_t> level_ptr; // family index ranges of equal set size
+  std::vector<int32_t> level_maxw;
+  std::vector<int32_t> w_host;
+  std::vector<int64_t> row_off_host;
+};
+
+struct rc_solution_s {
+  rc_family f = nullptr;
+  int64_t B = 0, Beff = 0;
+  int32_t objective = 0;
+  int32_t result = 0;             // RC_OK or RC_INFEASIBLE
+  int64_t t_star = -1, m_star = -1;
+  rcdp::Arena arena;
+  uint16_t* m = nullptr;          // [cells] opt values, kInfM = infinity
+  uint16_t* arg = nullptr;        // [cells] optarg family index, kNoArg = none
+  rcdp::DevStatus* status = nullptr;
+  int32_t* chain = nullptr;       // [F]
+  int32_t* seg = nullptr;         // [n]
+  uint8_t* cached = nullptr;      // [n]
+  hipEvent_t ev0 = nullptr, ev1 = nullptr;
+  float fill_ms = 0.f;
+};
+
+namespace rcdp {
+
+// ---- utilities (family.hip)
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);  // bytes % 8 == 0
+
+// ---- graph kernels (family.hip)
+hipError_t launch_graph_masks(rc_graph g, const int32_t* d_row_ptr, const int32_t* d_col_idx,
+                              hipStream_t s);
+
+// ---- family kernels (family.hip)
+hipError_t launch_ancestors(rc_graph g, uint64_t* anc, hipStream_t s);
+hipError_t launch_pruned_candidates(rc_graph g, const uint64_t* anc, uint64_t* cand,
+                                    hipStream_t s);
+hipError_t launch_enum_exact(rc_graph g, uint64_t* cand, int64_t cap, int32_t* lvl,
+                             DevStatus* st, hipStream_t s);
+hipError_t launch_rank(rc_graph g, int32_t mode, const uint64_t* cand, int64_t ncand_max,
+                       const int32_t* lvl, uint64_t* bits, int64_t fstride, DevStatus* st,
+                       hipStream_t s);
+hipError_t launch_set_quantities(rc_family f, hipStream_t s);
+hipError_t launch_pair_count(rc_family f, int64_t* counts, hipStream_t s);
+hipError_t launch_scan(const int64_t* in, int64_t* out, int64_t count, int64_t align,
+                       hipStream_t s);
+hipError_t launch_pair_write(rc_family f, int64_t* walg_per_target, hipStream_t s);
+hipError_t launch_row_widths(rc_family f, int64_t* padded, hipStream_t s);
+hipError_t launch_sum(const int64_t* in, int64_t count, int64_t* out, hipStream_t s);
+
+// ---- DP kernels (fill.hip)
+hipError_t launch_solve_init(rc_solution sol, hipStream_t s);
+hipError_t launch_fill(rc_solution sol, hipStream_t s);
+hipError_t launch_select(rc_solution sol, hipStream_t s);
+hipError_t launch_trace(rc_solution sol, hipStream_t s);
+
+}  // namespace rcdp

@@ -1,0 +1,176 @@
+"""GPU path versus the oracle, bit for bit (all quantities are integers).
+
+Every case runs the HIP library through its C ABI (rc_graph_create,
+rc_build_family, rc_solve, rc_reconstruct, rc_export_table) and the C
+oracle on the same seeded input, and compares: the family (members and
+order), the whole opt / optarg table over t = 0..T(V), t* and opt[V, t*]
+for both objectives, the traced chain, seg / cached, and the Eq. 1 / Eq. 2
+re-evaluation of the schedule.
+"""
+
+import numpy as np
+import pytest
+
+from paper_1905_11722_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def rc():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_1905_11722_amd import rcdp
+    rcdp.load_library()
+    return rcdp
+
+
+def compare(rc, O, g, mode, B, objectives=("tc", "mc"), table=True):
+    gg = rc.Graph.create(g)
+    fam = gg.build_family(mode)
+    ref = None
+    for objective in objectives:
+        ref = O.solve(g, mode, B, objective)
+        assert ref.status in (O.OK, O.INFEASIBLE), ref.status
+        sol = fam.solve(B, objective)
+        assert fam.info["num_sets"] == ref.num_sets
+        assert fam.info["num_pairs"] == ref.num_pairs
+        assert fam.info["T_total"] == ref.T_total
+        if ref.status == O.INFEASIBLE:
+            assert sol.status == rc.INFEASIBLE
+            assert (sol.t_star, sol.m_star) == (-1, -1)
+        else:
+            assert sol.status == rc.OK
+            assert (sol.t_star, sol.m_star) == (ref.t_star, ref.m_star)
+            sched = sol.reconstruct()
+            chain, seg, cached = ref.schedule()
+            np.testing.assert_array_equal(sched.chain, chain)
+            np.testing.assert_array_equal(sched.seg, seg)
+            np.testing.assert_array_equal(sched.cached, cached)
+            assert (sched.overhead, sched.peak, sched.cache_mem) == (
+                ref.overhead, ref.peak, ref.cache_mem)
+        if table:
+            m, a = sol.table()
+            rm, ra = ref.table()
+            np.testing.assert_array_equal(m, rm)
+            np.testing.assert_array_equal(a, ra)
+            table = False            # the table does not depend on the objective
+    np.testing.assert_array_equal(fam.sets(), ref.sets())
+    return fam
+
+
+SMALL = ["chain16", "ladder40"]
+
+
+@pytest.mark.parametrize("name", SMALL)
+def test_small_cases(rc, oracle_mod, name):
+    c = W.case(name)
+    g = c.graph
+    for B in (c.B, 2 * max(g.M), 2 * sum(g.M), 2 * sum(g.M) + 100):
+        compare(rc, oracle_mod, g, c.mode, B)
+
+
+def test_layered24_infeasible_and_feasible(rc, oracle_mod):
+    c = W.case("layered24")
+    g = c.graph
+    compare(rc, oracle_mod, g, "exact", c.B)           # no strategy at B = 256
+    for B in (900, 1200, 2 * sum(g.M)):
+        compare(rc, oracle_mod, g, "exact", B)
+        compare(rc, oracle_mod, g, "pruned", B)
+
+
+RANDOM = [(n, p, seed) for seed, (n, p) in enumerate(
+    [(n, p) for n in (2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12) for p in (0.1, 0.3, 0.5, 0.8)])]
+
+
+@pytest.mark.parametrize("n,p,seed", RANDOM)
+def test_random_dags(rc, oracle_mod, n, p, seed):
+    g = W.random_dag(n, p, 1000 + seed, tmax=40, mmax=30)
+    lo, hi = 2 * max(g.M), 2 * sum(g.M)
+    for B in (lo - 1, lo, (2 * lo + hi) // 3, (lo + hi) // 2, hi):
+        for mode in ("exact", "pruned"):
+            compare(rc, oracle_mod, g, mode, B)
+
+
+def test_wide_rows_many_tiles(rc, oracle_mod):
+    """Rows far wider than one kernel tile, with ragged tails."""
+    g = W.random_dag(9, 0.35, 77, tmax=900, mmax=40)
+    lo, hi = 2 * max(g.M), 2 * sum(g.M)
+    for B in (lo, (lo + hi) // 2, hi):
+        compare(rc, oracle_mod, g, "exact", B)
+        compare(rc, oracle_mod, g, "pruned", B)
+
+
+def test_antichain_wide_levels(rc, oracle_mod):
+    """Many independent targets per level (exact family of an antichain)."""
+    g = W.antichain(9, seed=4, tmax=30, mmax=20)
+    for B in (2 * max(g.M), sum(g.M), 2 * sum(g.M)):
+        compare(rc, oracle_mod, g, "exact", B)
+
+
+def test_empty_and_single(rc, oracle_mod):
+    g0 = W.Graph(0, [], [], [])
+    for mode in ("exact", "pruned"):
+        gg = rc.Graph.create(g0)
+        fam = gg.build_family(mode)
+        assert fam.info["num_sets"] == 1
+        sol = fam.solve(0, "tc")
+        assert (sol.status, sol.t_star, sol.m_star) == (rc.OK, 0, 0)
+        s = sol.reconstruct()
+        assert len(s.chain) == 0 and (s.overhead, s.peak, s.cache_mem) == (0, 0, 0)
+    g1 = W.chain(1, 3)
+    for B in (2 * g1.M[0] - 1, 2 * g1.M[0], 10 ** 6):
+        compare(rc, oracle_mod, g1, "exact", B)
+        compare(rc, oracle_mod, g1, "pruned", B)
+
+
+def test_budget_clamp_and_overflow(rc, oracle_mod):
+    g = W.chain(12, 5)
+    gg = rc.Graph.create(g)
+    fam = gg.build_family("exact")
+    a = fam.solve(2 * sum(g.M), "tc").table()
+    b = fam.solve(10 ** 9, "tc").table()               # clamped to 2 M(V)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+    big = W.Graph(2, [[1], []], [3, 4], [40000, 40000])
+    fb = rc.Graph.create(big).build_family("exact")
+    with pytest.raises(rc.RcError) as e:
+        fb.solve(10 ** 6, "tc")
+    assert e.value.status == rc.E_OVERFLOW
+    with pytest.raises(rc.RcError) as e:
+        rc.Graph.create(W.antichain(12)).build_family("exact", max_sets=4095)
+    assert e.value.status == rc.E_TOO_MANY_SETS
+
+
+def test_largest_exact_family(rc, oracle_mod):
+    """2^15 = 32768 lower sets (antichain of 15): the enumeration at scale."""
+    g = W.antichain(15, seed=1, tmax=3, mmax=3)
+    gg = rc.Graph.create(g)
+    fam = gg.build_family("exact")
+    assert fam.info["num_sets"] == 2 ** 15
+    sets = fam.sets()
+    vals = (sets * (1 << np.arange(15))).sum(axis=1)
+    sizes = sets.sum(axis=1)
+    order = np.lexsort((vals, sizes))
+    np.testing.assert_array_equal(order, np.arange(2 ** 15))
+    assert len(np.unique(vals)) == 2 ** 15
+
+
+def test_repeatable(rc, oracle_mod):
+    c = W.case("ladder40")
+    gg = rc.Graph.create(c.graph)
+    fam = gg.build_family("exact")
+    first = fam.solve(c.B, "tc").table()
+    for _ in range(3):
+        again = fam.solve(c.B, "tc").table()
+        np.testing.assert_array_equal(first[0], again[0])
+        np.testing.assert_array_equal(first[1], again[1])
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", ["resnet50", "unet", "densenet121"])
+def test_full_size_cases(rc, oracle_mod, name):
+    """The CNN-shaped cases at full size, whole table."""
+    c = W.case(name)
+    compare(rc, oracle_mod, c.graph, c.mode, c.B)
