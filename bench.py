@@ -27,7 +27,8 @@ if ROOT not in sys.path:
 # MI355X: 256 CUs, 64 int32 lanes per CU per clock, 2.4 GHz peak engine clock.
 VALU_INT32_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
 OPS_PER_RELAXATION = 3          # compare with tau, add dm, min into the target
-FILL_SOURCES = ["paper_1905_11722_amd/csrc/fill.hip"]
+FILL_SOURCES = ["paper_1905_11722_amd/csrc/fill.hip", "paper_1905_11722_amd/csrc/blocked.hip",
+                "paper_1905_11722_amd/csrc/blocks.hip"]
 
 
 def fill_source_hash():
@@ -188,7 +189,7 @@ def main():
             "unit": "TOP/s (int32 VALU)",
             "frac": achieved / VALU_INT32_PEAK_TOPS,
             "traffic": read_traffic(case.name),
-            "kernel": "k_fill_level (all launches of one solve)",
+            "kernel": "DP fill of one solve (k_fill_blocked, or k_fill_level launches)",
             "ops_per_relaxation": OPS_PER_RELAXATION,
         },
         "per_graph": per_graph,

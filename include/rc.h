@@ -180,6 +180,10 @@ void rc_solution_free(rc_solution s);
 
 /* Static description of a status code. */
 const char* rc_status_str(int status);
+/* Description of the last RC_E_DEVICE returned on the calling thread (the
+ * failing HIP call and its error string, or the kernel-reported condition);
+ * empty when none.  Valid until the next call on that thread. */
+const char* rc_last_error(void);
 
 #ifdef __cplusplus
 }

@@ -304,6 +304,17 @@ __global__ void k_row_widths(int64_t F, const int32_t* w, int64_t* padded) {
   if (s < F) padded[s] = ((int64_t)w[s] + kRowAlign - 1) / kRowAlign * kRowAlign;
 }
 
+// Rows are right-aligned inside their padded slots: row s ends on a
+// kRowAlign boundary, so every column counted from the row end is made of
+// whole 128-byte lines.
+__global__ void k_row_align(int64_t F, const int32_t* w, int64_t* row_off) {
+  const int64_t s = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (s < F) {
+    const int64_t pad = ((int64_t)w[s] + kRowAlign - 1) / kRowAlign * kRowAlign;
+    row_off[s] += pad - w[s];
+  }
+}
+
 // ------------------------------------------------------------------ pairs
 
 // Subset test of family members i and j (word-major storage).
@@ -502,6 +513,12 @@ hipError_t launch_set_quantities(rc_family f, hipStream_t s) {
 hipError_t launch_row_widths(rc_family f, int64_t* padded, hipStream_t s) {
   hipLaunchKernelGGL(k_row_widths, dim3((unsigned)((f->F + 255) / 256)), dim3(256), 0, s, f->F,
                      f->w, padded);
+  return hipGetLastError();
+}
+
+hipError_t launch_row_align(rc_family f, hipStream_t s) {
+  hipLaunchKernelGGL(k_row_align, dim3((unsigned)((f->F + 255) / 256)), dim3(256), 0, s, f->F,
+                     f->w, f->row_off);
   return hipGetLastError();
 }
 

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <vector>
@@ -12,12 +14,26 @@
 
 using namespace rcdp;
 
-#define RC_HIP(x)                              \
-  do {                                         \
-    if ((x) != hipSuccess) return RC_E_DEVICE; \
+#define RC_HIP(x)                                     \
+  do {                                                \
+    hipError_t e_ = (x);                              \
+    if (e_ != hipSuccess) {                           \
+      rcdp::set_last_error(#x, e_);                   \
+      return RC_E_DEVICE;                             \
+    }                                                 \
   } while (0)
 
 namespace rcdp {
+
+static thread_local char g_last_error[512] = "";
+
+void set_last_error(const char* what, hipError_t e) {
+  std::snprintf(g_last_error, sizeof(g_last_error), "%s: %s", what, hipGetErrorString(e));
+}
+
+void set_last_error_msg(const char* msg) {
+  std::snprintf(g_last_error, sizeof(g_last_error), "%s", msg);
+}
 
 void* Arena::get(size_t bytes) {
   if (bytes == 0) bytes = 1;
@@ -57,6 +73,8 @@ static int upload(Arena& a, const T* host, int64_t count, T** dev, hipStream_t s
 }
 
 extern "C" {
+
+const char* rc_last_error(void) { return g_last_error; }
 
 const char* rc_status_str(int status) {
   switch (status) {
@@ -263,6 +281,7 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
   // row offsets: rows padded to kRowAlign cells
   RC_HIP(launch_row_widths(f, padded, s));
   RC_HIP(launch_scan(padded, f->row_off, F, 1, s));
+  RC_HIP(launch_row_align(f, s));
 
   // ---- a4: predecessor pairs
   RC_HIP(launch_pair_count(f, counts, s));
@@ -279,6 +298,14 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
   if (!f->pidx || !f->pdt || !f->pdm || !f->pc) return RC_E_NOMEM;
   RC_HIP(launch_pair_write(f, walg_t, s));
   RC_HIP(launch_sum(walg_t, F, &f->status->walg, s));
+  // records of the blocked fill: one per (block of kJB targets, panel source)
+  f->nblk = (F - 1 + kJB - 1) / kJB;
+  if (f->nblk > 0) {
+    f->rec_ptr = A.get_n<int64_t>(f->nblk + 1);
+    if (!f->rec_ptr) return RC_E_NOMEM;
+    RC_HIP(launch_blk_count(f, f->nblk, counts, s));
+    RC_HIP(launch_scan(counts, f->rec_ptr, f->nblk, 1, s));
+  }
 
   // ---- host copies for launch configuration
   std::vector<int32_t> size_h(F);
@@ -289,9 +316,34 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
   RC_HIP(hipMemcpyAsync(f->row_off_host.data(), f->row_off, sizeof(int64_t) * (F + 1),
                         hipMemcpyDeviceToHost, s));
   RC_HIP(hipMemcpyAsync(&hs, f->status, sizeof(hs), hipMemcpyDeviceToHost, s));
+  f->rec_total = 0;
+  if (f->nblk > 0)
+    RC_HIP(hipMemcpyAsync(&f->rec_total, f->rec_ptr + f->nblk, sizeof(int64_t),
+                          hipMemcpyDeviceToHost, s));
   RC_HIP(hipStreamSynchronize(s));
   if (hs.error) return RC_E_DEVICE;
   f->relax = hs.walg;
+  f->has_records = false;
+  if (f->nblk > 0 && f->rec_total <= kMaxRecords) {
+    BlockRecords& R = f->rec;
+    const int64_t Rn = f->rec_total, T3 = f->nblk * kJB * kJB;
+    R.src = A.get_n<int32_t>(Rn);
+    R.emin = A.get_n<int32_t>(Rn);
+    R.emax = A.get_n<int32_t>(Rn);
+    R.e = A.get_n<int32_t>(Rn * kJB);
+    R.kadd = A.get_n<uint32_t>(Rn * kJB);
+    R.c = A.get_n<int32_t>(Rn * kJB);
+    R.tri_e = A.get_n<int32_t>(T3);
+    R.tri_kadd = A.get_n<uint32_t>(T3);
+    R.tri_c = A.get_n<int32_t>(T3);
+    R.tri_emax = A.get_n<int32_t>(f->nblk * kJB);
+    R.blk_emax = A.get_n<int32_t>(f->nblk);
+    if (!R.src || !R.emin || !R.emax || !R.e || !R.kadd || !R.c || !R.tri_e || !R.tri_kadd ||
+        !R.tri_c || !R.tri_emax || !R.blk_emax)
+      return RC_E_NOMEM;
+    RC_HIP(launch_blk_fill(f, f->nblk, s));
+    f->has_records = true;
+  }
   f->cells = f->row_off_host[F];
   if (f->cells >= ((int64_t)1 << 40)) return RC_E_OVERFLOW;
   f->level_ptr.clear();
@@ -370,6 +422,19 @@ void rc_family_free(rc_family f) {
 
 // ------------------------------------------------------------------ solve
 
+// Level launches suit narrow tables (few columns, many targets per level);
+// the persistent wavefront suits wide ones.  RCDP_FILL=level|wavefront
+// overrides the choice.
+static int choose_fill_path(rc_family f) {
+  if (!f->has_records || f->F < 2) return 0;
+  const char* env = std::getenv("RCDP_FILL");
+  if (env && std::strcmp(env, "level") == 0) return 0;
+  if (env && std::strcmp(env, "wavefront") == 0) return 1;
+  // many sequential levels over wide rows: one persistent launch beats one
+  // launch per level; few levels over wide rows: the level launches win
+  return (f->max_row >= 8192 && f->level_ptr.size() > 100) ? 1 : 0;
+}
+
 int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solution* out,
              int64_t* t_opt, int64_t* m_opt) {
   if (!f || !out || B < 0) return RC_E_ARG;
@@ -404,16 +469,35 @@ int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solutio
     return fail(RC_E_NOMEM);
   if (hipEventCreate(&sol->ev0) != hipSuccess || hipEventCreate(&sol->ev1) != hipSuccess)
     return fail(RC_E_DEVICE);
+  sol->fill_path = choose_fill_path(f);
+  if (sol->fill_path == 1) {
+    sol->progress = sol->arena.get_n<int32_t>(blocked_columns(f));
+    sol->ticket = sol->arena.get_n<int32_t>(1);
+    if (!sol->progress || !sol->ticket) return fail(RC_E_NOMEM);
+  }
   if (launch_solve_init(sol, s) != hipSuccess) return fail(RC_E_DEVICE);
   if (hipEventRecord(sol->ev0, s) != hipSuccess) return fail(RC_E_DEVICE);
-  if (launch_fill(sol, s) != hipSuccess) return fail(RC_E_DEVICE);
+  hipError_t fe = hipSuccess;
+  if (sol->fill_path == 1) {
+    fe = launch_fill_blocked(sol, s);
+  } else {
+    fe = launch_fill(sol, s);
+  }
+  if (fe != hipSuccess) {
+    set_last_error(sol->fill_path == 1 ? "blocked fill launch" : "level fill launch", fe);
+    return fail(RC_E_DEVICE);
+  }
   if (hipEventRecord(sol->ev1, s) != hipSuccess) return fail(RC_E_DEVICE);
   if (launch_select(sol, s) != hipSuccess) return fail(RC_E_DEVICE);
   DevStatus hs;
   if (hipMemcpyAsync(&hs, sol->status, sizeof(hs), hipMemcpyDeviceToHost, s) != hipSuccess ||
       hipStreamSynchronize(s) != hipSuccess)
     return fail(RC_E_DEVICE);
-  if (hs.error) return fail(RC_E_DEVICE);
+  if (hs.error) {
+    set_last_error_msg(hs.error == 3 ? "blocked fill: a wait timed out (kernel aborted)"
+                                     : "DP fill kernel reported an inconsistency");
+    return fail(RC_E_DEVICE);
+  }
   if (hipEventElapsedTime(&sol->fill_ms, sol->ev0, sol->ev1) != hipSuccess) sol->fill_ms = -1.f;
   sol->t_star = hs.t_sel;
   sol->m_star = hs.t_sel >= 0 ? hs.m_sel : -1;
@@ -449,7 +533,10 @@ int rc_reconstruct(rc_solution sol, void* stream, int32_t* k, int32_t* chain_hos
     RC_HIP(hipMemcpyAsync(ca.data(), sol->cached, n, hipMemcpyDeviceToHost, s));
   }
   RC_HIP(hipStreamSynchronize(s));
-  if (hs.error || hs.k < 0 || hs.k > f->F) return RC_E_DEVICE;
+  if (hs.error || hs.k < 0 || hs.k > f->F) {
+    set_last_error_msg("traceback: optarg walk did not end at (empty set, 0)");
+    return RC_E_DEVICE;
+  }
   if (k) *k = hs.k;
   if (chain_host) std::copy(ch.begin(), ch.begin() + hs.k, chain_host);
   if (seg_host) std::copy(sg.begin(), sg.end(), seg_host);

@@ -18,6 +18,8 @@ constexpr int kMaxSets = 65535;                 // family index fits 16 bits
 constexpr uint32_t kInfM = 0xFFFFu;             // opt = infinity in a 16-bit cell
 constexpr uint32_t kNoArg = 0xFFFFu;            // optarg = none
 constexpr int64_t kRowAlign = 64;               // cells; rows start on 128-byte lines
+constexpr int kJB = 8;                          // blocked fill: targets per block
+constexpr int64_t kMaxRecords = (int64_t)1 << 21;  // blocked fill: cap on panel records
 
 // Device allocator with ownership tracking.
 struct Arena {
@@ -43,6 +45,21 @@ struct DevStatus {
   int32_t k;             // chain length
   int32_t pad0;
   int64_t overhead, peak, cache_mem;
+};
+
+// Panel / triangle records of the blocked fill (blocks.hip).
+struct BlockRecords {
+  int32_t* src = nullptr;       // [R] source family index
+  int32_t* emin = nullptr;      // [R] smallest shift among the record's slots
+  int32_t* emax = nullptr;      // [R] largest shift
+  int32_t* e = nullptr;         // [R * kJB] shift of (src, j0 + slot), -1 = no pair
+  uint32_t* kadd = nullptr;     // [R * kJB] (dm << 16) | src
+  int32_t* c = nullptr;         // [R * kJB] budget term
+  int32_t* tri_e = nullptr;     // [nblk * kJB * kJB] in-block pairs (row slot, target slot)
+  uint32_t* tri_kadd = nullptr;
+  int32_t* tri_c = nullptr;
+  int32_t* tri_emax = nullptr;  // [nblk * kJB] largest shift out of each in-block row, -1 none
+  int32_t* blk_emax = nullptr;  // [nblk] largest panel shift of the block
 };
 
 }  // namespace rcdp
@@ -79,6 +96,12 @@ struct rc_family_s {
   // device: predecessor pairs, CSR by target
   int64_t* pred_ptr = nullptr;    // [F+1]
   int32_t *pidx = nullptr, *pdt = nullptr, *pdm = nullptr, *pc = nullptr;
+  // blocked fill: records per block of kJB targets (absent when too large)
+  int64_t nblk = 0;
+  int64_t rec_total = 0;
+  bool has_records = false;
+  int64_t* rec_ptr = nullptr;     // [nblk+1]
+  rcdp::BlockRecords rec;
   rcdp::DevStatus* status = nullptr;
   // host copies used for launches
   std::vector<int64_t> level_ptr; // family index ranges of equal set size
@@ -100,11 +123,18 @@ struct rc_solution_s {
   int32_t* chain = nullptr;       // [F]
   int32_t* seg = nullptr;         // [n]
   uint8_t* cached = nullptr;      // [n]
+  int32_t* progress = nullptr;    // blocked fill: rows finished per column
+  int32_t* ticket = nullptr;      // blocked fill: next column to take
+  int32_t fill_path = 0;          // 0 level launches, 1 blocked wavefront
   hipEvent_t ev0 = nullptr, ev1 = nullptr;
   float fill_ms = 0.f;
 };
 
 namespace rcdp {
+
+// Thread-local description of the last RC_E_DEVICE (rc_api.hip).
+void set_last_error(const char* what, hipError_t e);
+void set_last_error_msg(const char* msg);
 
 // ---- utilities (family.hip)
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);  // bytes % 8 == 0
@@ -135,5 +165,13 @@ hipError_t launch_solve_init(rc_solution sol, hipStream_t s);
 hipError_t launch_fill(rc_solution sol, hipStream_t s);
 hipError_t launch_select(rc_solution sol, hipStream_t s);
 hipError_t launch_trace(rc_solution sol, hipStream_t s);
+
+// ---- blocked fill (blocks.hip, blocked.hip)
+hipError_t launch_row_align(rc_family f, hipStream_t s);
+hipError_t launch_blk_count(rc_family f, int64_t nblk, int64_t* count, hipStream_t s);
+hipError_t launch_blk_fill(rc_family f, int64_t nblk, hipStream_t s);
+int blocked_cells_per_thread(rc_family f);
+int64_t blocked_columns(rc_family f);
+hipError_t launch_fill_blocked(rc_solution sol, hipStream_t s);
 
 }  // namespace rcdp

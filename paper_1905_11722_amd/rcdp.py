@@ -38,7 +38,10 @@ FREE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p)
 class RcError(RuntimeError):
     def __init__(self, status, where):
         self.status = status
-        super().__init__(f"{where}: status {status} ({status_str(status)})")
+        detail = ""
+        if status == E_DEVICE:
+            detail = ": " + load_library().rc_last_error().decode(errors="replace")
+        super().__init__(f"{where}: status {status} ({status_str(status)}){detail}")
 
 
 class FamilyInfo(ctypes.Structure):
@@ -68,6 +71,8 @@ def load_library():
     pp = ctypes.POINTER(ctypes.c_void_p)
     lib.rc_status_str.restype = ctypes.c_char_p
     lib.rc_status_str.argtypes = [ctypes.c_int]
+    lib.rc_last_error.restype = ctypes.c_char_p
+    lib.rc_last_error.argtypes = []
     lib.rc_graph_create.restype = ctypes.c_int
     lib.rc_graph_create.argtypes = [i32, P, P, P, P, ALLOC_FN, FREE_FN, P, P, pp]
     lib.rc_graph_free.argtypes = [P]

@@ -174,3 +174,42 @@ def test_full_size_cases(rc, oracle_mod, name):
     """The CNN-shaped cases at full size, whole table."""
     c = W.case(name)
     compare(rc, oracle_mod, c.graph, c.mode, c.B)
+
+
+# ---------------------------------------------------------------- fill paths
+# The library picks the persistent wavefront fill for wide tables and
+# per-level launches for narrow ones; RCDP_FILL forces either.  Rows wider
+# than one 512-cell column make the wavefront's cross-workgroup waits real.
+
+WIDE = [(n, p, seed) for seed, (n, p) in enumerate(
+    [(n, p) for n in (4, 6, 8, 10, 12) for p in (0.2, 0.45, 0.7)])]
+
+
+@pytest.mark.parametrize("path", ["level", "wavefront"])
+@pytest.mark.parametrize("n,p,seed", WIDE)
+def test_fill_paths_wide_rows(rc, oracle_mod, monkeypatch, path, n, p, seed):
+    monkeypatch.setenv("RCDP_FILL", path)
+    g = W.random_dag(n, p, 5000 + seed, tmax=700, mmax=60)
+    lo, hi = 2 * max(g.M), 2 * sum(g.M)
+    for B in (lo, (2 * lo + hi) // 3, hi):
+        for mode in ("exact", "pruned"):
+            compare(rc, oracle_mod, g, mode, B)
+
+
+@pytest.mark.parametrize("path", ["level", "wavefront"])
+@pytest.mark.parametrize("name", SMALL + ["layered24"])
+def test_fill_paths_small_cases(rc, oracle_mod, monkeypatch, path, name):
+    monkeypatch.setenv("RCDP_FILL", path)
+    c = W.case(name)
+    g = c.graph
+    for B in (c.B, 2 * max(g.M), sum(g.M), 2 * sum(g.M)):
+        compare(rc, oracle_mod, g, c.mode, B)
+
+
+@pytest.mark.parametrize("path", ["level", "wavefront"])
+def test_fill_paths_long_chain(rc, oracle_mod, monkeypatch, path):
+    """A long chain: one target per level, rows of many columns."""
+    monkeypatch.setenv("RCDP_FILL", path)
+    g = W.chain(60, seed=9, tmax=400, mmax=30)
+    for B in (2 * max(g.M), sum(g.M) // 3, sum(g.M), 2 * sum(g.M)):
+        compare(rc, oracle_mod, g, "exact", B)
