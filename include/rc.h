@@ -142,7 +142,7 @@ void rc_family_free(rc_family f);
  *    RC_MEMORY_CENTRIC: t* = max{t : opt[V, t] finite} (Section 4.4).
  *  *t_opt, *m_opt: t* and opt[V, t*], or -1 and -1 when infeasible.
  * Returns RC_OK or RC_INFEASIBLE (both create *out, whose table can be
- * exported), or an error: RC_E_ARG, RC_E_OVERFLOW (min(B, 2 M(V)) > 65534),
+ * exported), or an error: RC_E_ARG, RC_E_OVERFLOW (min(B, 2 M(V)) > 65532),
  * RC_E_NOMEM, RC_E_DEVICE.
  */
 int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solution* out,

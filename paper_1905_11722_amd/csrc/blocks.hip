@@ -17,6 +17,8 @@
 // and one window of source row i serves every target of the block.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "rc_internal.h"
 
 namespace rcdp {
@@ -59,14 +61,8 @@ __global__ __launch_bounds__(256) void k_blk_fill(int64_t F, const int32_t* w,
   const int words = (int)((j0 + 31) / 32);
   const int64_t base = rec_ptr[b], nrec = rec_ptr[b + 1] - base;
   for (int x = threadIdx.x; x < words; x += blockDim.x) bitmap[x] = 0;
-  for (int64_t r = threadIdx.x; r < nrec; r += blockDim.x) {
-    R.emin[base + r] = INT32_MAX;
-    R.emax[base + r] = -1;
-    for (int s = 0; s < kJB; s++) R.e[(base + r) * kJB + s] = -1;
-  }
+  for (int64_t x = threadIdx.x; x < nrec * kJB; x += blockDim.x) R.e[base * kJB + x] = -1;
   for (int x = threadIdx.x; x < kJB * kJB; x += blockDim.x) R.tri_e[b * kJB * kJB + x] = -1;
-  for (int x = threadIdx.x; x < kJB; x += blockDim.x) R.tri_emax[b * kJB + x] = -1;
-  if (threadIdx.x == 0) R.blk_emax[b] = 0;
   __syncthreads();
   for (int64_t j = j0; j < j1; j++)
     for (int64_t q = pred_ptr[j] + threadIdx.x; q < pred_ptr[j + 1]; q += blockDim.x) {
@@ -74,14 +70,25 @@ __global__ __launch_bounds__(256) void k_blk_fill(int64_t F, const int32_t* w,
       if (i < j0) atomicOr(&bitmap[i >> 5], 1u << (i & 31));
     }
   __syncthreads();
-  if (threadIdx.x == 0) {              // exclusive prefix of popcounts
-    int32_t run = 0;
-    for (int x = 0; x < words; x++) {
-      prefix[x] = run;
-      run += __popc(bitmap[x]);
+  // exclusive prefix of the popcounts, 256 words per pass
+  __shared__ int32_t s_wsum[4];
+  int32_t carry = 0;
+  for (int w0 = 0; w0 < words; w0 += 256) {
+    const int x = w0 + (int)threadIdx.x;
+    const int32_t v = x < words ? __popc(bitmap[x]) : 0;
+    int32_t incl = v;
+    for (int off = 1; off < 64; off <<= 1) {
+      const int32_t y = __shfl_up(incl, off, 64);
+      if ((threadIdx.x & 63) >= off) incl += y;
     }
+    if ((threadIdx.x & 63) == 63) s_wsum[threadIdx.x / 64] = incl;
+    __syncthreads();
+    int32_t before = carry;
+    for (int q = 0; q < (int)threadIdx.x / 64; q++) before += s_wsum[q];
+    if (x < words) prefix[x] = before + incl - v;
+    carry += s_wsum[0] + s_wsum[1] + s_wsum[2] + s_wsum[3];
+    __syncthreads();
   }
-  __syncthreads();
   for (int64_t j = j0; j < j1; j++) {
     const int slot = (int)(j - j0);
     for (int64_t q = pred_ptr[j] + threadIdx.x; q < pred_ptr[j + 1]; q += blockDim.x) {
@@ -96,15 +103,11 @@ __global__ __launch_bounds__(256) void k_blk_fill(int64_t F, const int32_t* w,
         R.e[r * kJB + slot] = e;
         R.kadd[r * kJB + slot] = kadd;
         R.c[r * kJB + slot] = pc[q];
-        atomicMin(&R.emin[r], e);
-        atomicMax(&R.emax[r], e);
-        atomicMax(&R.blk_emax[b], e);
       } else {
         const int64_t t = b * kJB * kJB + (int64_t)(i - j0) * kJB + slot;
         R.tri_e[t] = e;
         R.tri_kadd[t] = kadd;
         R.tri_c[t] = pc[q];
-        atomicMax(&R.tri_emax[b * kJB + (i - j0)], e);
       }
     }
   }
@@ -121,6 +124,400 @@ hipError_t launch_blk_count(rc_family f, int64_t nblk, int64_t* count, hipStream
 hipError_t launch_blk_fill(rc_family f, int64_t nblk, hipStream_t s) {
   hipLaunchKernelGGL(k_blk_fill, dim3((unsigned)nblk), dim3(256), 0, s, f->F, f->w, f->pred_ptr,
                      f->pidx, f->pdt, f->pdm, f->pc, f->rec_ptr, f->rec);
+  return hipGetLastError();
+}
+
+}  // namespace rcdp
+
+namespace rcdp {
+
+namespace {
+
+// Shift clusters of a record: its slots sorted by shift, cut wherever the
+// shift exceeds the first shift of the current cluster by more than kSpan.
+// Each cluster becomes one compact record, so a staged window of
+// C + kSpan cells serves every slot of it.  Returns the count and fills
+// cl[s] (cluster number of slot s, -1 without a pair).
+__device__ int record_clusters(const int32_t* e, int32_t* cl) {
+  int32_t order[kJB];
+  int n = 0;
+  for (int s = 0; s < kJB; s++) {
+    cl[s] = -1;
+    if (e[s] >= 0) order[n++] = s;
+  }
+  for (int x = 1; x < n; x++)            // insertion sort by shift
+    for (int y = x; y > 0 && e[order[y]] < e[order[y - 1]]; y--) {
+      const int32_t t = order[y];
+      order[y] = order[y - 1];
+      order[y - 1] = t;
+    }
+  int ncl = 0;
+  int32_t first = 0;
+  for (int x = 0; x < n; x++) {
+    const int32_t ev = e[order[x]];
+    if (x == 0 || ev - first > kSpan) {
+      first = ev;
+      ncl++;
+    }
+    cl[order[x]] = ncl - 1;
+  }
+  return ncl;
+}
+
+// Compact records per block (B-independent upper bound for every solve).
+__global__ __launch_bounds__(256) void k_blk_clusters(const int64_t* rec_ptr, BlockRecords R,
+                                                      int64_t* count) {
+  const int64_t b = blockIdx.x;
+  __shared__ int64_t s_n;
+  if (threadIdx.x == 0) s_n = 0;
+  __syncthreads();
+  int64_t n = 0;
+  for (int64_t r = rec_ptr[b] + threadIdx.x; r < rec_ptr[b + 1]; r += blockDim.x) {
+    int32_t cl[kJB];
+    n += record_clusters(R.e + r * kJB, cl);
+  }
+  atomicAdd((unsigned long long*)&s_n, (unsigned long long)n);
+  __syncthreads();
+  if (threadIdx.x == 0) count[b] = s_n;
+}
+
+// Per solve, panel records: keep the slots whose budget test can pass
+// (pair exists and B - c >= 0) of the records whose source lies before the
+// previous block (sources i < max(j0 - kJB, 1); the previous block's rows
+// reach the block through row pushes instead), and emit one compact record
+// per shift cluster that has such a slot, compacted from clu_ptr[b] on.  A
+// compact record is kRecInts int32: [0] source i, [1] smallest shift emin,
+// [2] staged span emax - emin (<= kSpan), [3] P_i = w_i - 1, [4..5] index of
+// the cell u = 0 of row i (int64), [6] emax, [8 + s] shift - emin of slot s,
+// [16 + p] budgets B - c of slots 2p, 2p+1 as two uint16, [20 + p] the
+// additions dm of slots 2p, 2p+1 as two uint16.  A slot without a live pair
+// gets budget 0 and addition 0xFFFF, so its candidate always saturates to
+// infinity.  meta[b * kMetaInts] = {records, largest live shift, rows of
+// the block, largest P of its rows, ...}.
+__global__ __launch_bounds__(256) void k_rec_prepare(int64_t F, int32_t Beff, const int32_t* w,
+                                                     const int64_t* row_off,
+                                                     const int64_t* rec_ptr,
+                                                     const int64_t* clu_ptr, BlockRecords R,
+                                                     int32_t* crec, int32_t* meta) {
+  const int64_t b = blockIdx.x;
+  const int64_t base = rec_ptr[b], n = rec_ptr[b + 1] - base;
+  const int64_t obase = clu_ptr[b];
+  const int64_t j0 = 1 + b * kJB;
+  const int64_t old_end = j0 - kJB > 1 ? j0 - kJB : 1;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x / 64;
+  __shared__ int32_t s_wcnt[4];
+  __shared__ int32_t s_run, s_emax;
+  if (threadIdx.x == 0) {
+    s_run = 0;
+    s_emax = 0;
+  }
+  __syncthreads();
+  for (int64_t r0 = 0; r0 < n; r0 += 256) {
+    const int64_t r = r0 + threadIdx.x;
+    int32_t e[kJB], cl[kJB];
+    int ncl = 0;
+    uint32_t live_cl = 0;                  // clusters with a live slot
+    if (r < n && R.src[base + r] < old_end) {
+      for (int s = 0; s < kJB; s++) e[s] = R.e[(base + r) * kJB + s];
+      ncl = record_clusters(e, cl);
+      for (int s = 0; s < kJB; s++)
+        if (cl[s] >= 0 && Beff - R.c[(base + r) * kJB + s] >= 0) live_cl |= 1u << cl[s];
+    }
+    const int mine = __popc(live_cl);
+    int incl = mine;                       // inclusive prefix over the workgroup
+    for (int off = 1; off < 64; off <<= 1) {
+      const int y = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += y;
+    }
+    if (lane == 63) s_wcnt[wave] = incl;
+    __syncthreads();
+    int32_t o = s_run + incl - mine;
+    for (int q = 0; q < wave; q++) o += s_wcnt[q];
+    for (int k = 0; k < ncl; k++) {
+      if (!(live_cl & (1u << k))) continue;
+      int32_t* d = crec + (obase + o) * kRecInts;
+      const int32_t i = R.src[base + r];
+      const int32_t Pi = w[i] - 1;
+      const int64_t endi = row_off[i] + Pi;
+      int32_t emin = INT32_MAX, emax = -1;
+      for (int s = 0; s < kJB; s++)
+        if (cl[s] == k) {
+          emin = min(emin, e[s]);
+          emax = max(emax, e[s]);
+        }
+      uint32_t tau2[kJB / 2] = {0, 0, 0, 0}, dm2[kJB / 2] = {0, 0, 0, 0};
+      for (int s = 0; s < kJB; s++) {
+        const int32_t tau = Beff - R.c[(base + r) * kJB + s];
+        const bool ok = cl[s] == k && tau >= 0;
+        d[8 + s] = ok ? e[s] - emin : 0;
+        const uint32_t tv = ok ? (uint32_t)tau : 0u;
+        const uint32_t dv = ok ? (R.kadd[(base + r) * kJB + s] >> 16) : 0xFFFFu;
+        tau2[s / 2] |= tv << (16 * (s & 1));
+        dm2[s / 2] |= dv << (16 * (s & 1));
+      }
+      d[0] = i;
+      d[1] = emin;
+      d[2] = emax - emin;
+      d[3] = Pi;
+      d[4] = (int32_t)(endi & 0xFFFFFFFF);
+      d[5] = (int32_t)(endi >> 32);
+      d[6] = emax;
+      d[7] = 0;
+      for (int x = 0; x < kJB / 2; x++) {
+        d[16 + x] = (int32_t)tau2[x];
+        d[20 + x] = (int32_t)dm2[x];
+      }
+      for (int x = 24; x < kRecInts; x++) d[x] = 0;
+      atomicMax(&s_emax, emax);
+      o++;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int32_t t = 0;
+      for (int q = 0; q < 4; q++) t += s_wcnt[q];
+      s_run += t;
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const int64_t j1 = j0 + kJB < F ? j0 + kJB : F;
+    int32_t mp = -1;
+    for (int64_t j = j0; j < j1; j++) mp = max(mp, w[j] - 1);
+    int32_t* mt = meta + b * kMetaInts;
+    mt[0] = s_run;                      // live panel records
+    mt[1] = s_emax;                     // largest live panel shift
+    mt[2] = (int32_t)(j1 - j0);         // rows of the block
+    mt[3] = mp;                         // largest P of the block's rows
+    for (int x = 4; x < kMetaInts; x++) mt[x] = 0;
+  }
+}
+
+// Per solve, row pushes: for row s of block b (source j = j0 + s) the
+// targets are the later rows of the block (slots 0..7, only s2 > s) and the
+// rows of block b + 1 (slots 8..15).  A live target (pair exists, B - c >= 0)
+// with shift e <= kHalo reads the source row buffer at offset e (own column
+// plus halo); a larger shift gets a staged window of its own.  List layout
+// (kPushInts int32): [0] halo cells (largest near shift rounded up to 8),
+// [1] far windows, [2] largest P over live targets (-1 none), [3] largest
+// live shift, [4] P_j, [5..6] index of the cell u = 0 of row j, [8 + k] the
+// shift of far window k, [24 + p] LDS cell offsets of targets 2p, 2p+1 as
+// two uint16 (near: e, relative to the row buffer; far: 2 RB + k FB + e % 8
+// with RB = C + kHalo + 8, FB = C + 8), [32 + p] budgets and [40 + p]
+// additions of targets 2p, 2p+1 as two uint16 (dead: 0 and 0xFFFF).
+__global__ __launch_bounds__(64) void k_push_prepare(int64_t F, int64_t nblk, int32_t Beff,
+                                                     int32_t C, const int32_t* w,
+                                                     const int64_t* row_off,
+                                                     const int64_t* rec_ptr, BlockRecords R,
+                                                     int32_t* push) {
+  const int64_t b = blockIdx.x;
+  const int s = threadIdx.x;
+  if (s >= kJB) return;
+  const int64_t j0 = 1 + b * kJB;
+  const int64_t j = j0 + s;
+  int32_t* d = push + (b * kJB + s) * kPushInts;
+  int32_t e[2 * kJB], tau[2 * kJB], dm[2 * kJB];
+  for (int t = 0; t < 2 * kJB; t++) {
+    e[t] = -1;
+    tau[t] = 0;
+    dm[t] = 0xFFFF;
+  }
+  if (j < F) {
+    for (int s2 = s + 1; s2 < kJB && j0 + s2 < F; s2++) {      // later rows of the block
+      const int64_t x = b * kJB * kJB + s * kJB + s2;
+      const int32_t tv = Beff - R.tri_c[x];
+      if (R.tri_e[x] >= 0 && tv >= 0) {
+        e[s2] = R.tri_e[x];
+        tau[s2] = tv;
+        dm[s2] = (int32_t)(R.tri_kadd[x] >> 16);
+      }
+    }
+    if (b + 1 < nblk) {                   // rows of the next block: its record of source j
+      for (int64_t r = rec_ptr[b + 2] - 1; r >= rec_ptr[b + 1] && R.src[r] >= j0; r--) {
+        if (R.src[r] != j) continue;
+        for (int s2 = 0; s2 < kJB; s2++) {
+          const int32_t ev = R.e[r * kJB + s2];
+          const int32_t tv = Beff - R.c[r * kJB + s2];
+          if (ev >= 0 && tv >= 0) {
+            e[kJB + s2] = ev;
+            tau[kJB + s2] = tv;
+            dm[kJB + s2] = (int32_t)(R.kadd[r * kJB + s2] >> 16);
+          }
+        }
+        break;
+      }
+    }
+  }
+  const int32_t RB = C + kHalo + 8, FB = C + 8;
+  int32_t hs = 0, nfar = 0, maxPt = -1, emax = -1;
+  int32_t off[2 * kJB];
+  for (int x = 0; x < 2 * kPushInts / 2; x++) d[x] = 0;
+  for (int t = 0; t < 2 * kJB; t++) {
+    off[t] = 0;
+    if (e[t] < 0) continue;
+    const int64_t jt = t < kJB ? j0 + t : j0 + kJB + (t - kJB);
+    maxPt = max(maxPt, w[jt] - 1);
+    emax = max(emax, e[t]);
+    if (e[t] <= kHalo) {
+      off[t] = e[t];
+      hs = max(hs, (e[t] + 7) / 8 * 8);
+    } else {
+      d[8 + nfar] = e[t];
+      off[t] = 2 * RB + nfar * FB + (e[t] & 7);
+      nfar++;
+    }
+  }
+  d[0] = hs;
+  d[1] = nfar;
+  d[2] = maxPt;
+  d[3] = emax;
+  const int32_t Pj = j < F ? w[j] - 1 : -1;
+  const int64_t endj = j < F ? row_off[j] + Pj : 0;
+  d[4] = Pj;
+  d[5] = (int32_t)(endj & 0xFFFFFFFF);
+  d[6] = (int32_t)(endj >> 32);
+  for (int p = 0; p < kJB; p++) {
+    d[24 + p] = (int32_t)((uint32_t)off[2 * p] | ((uint32_t)off[2 * p + 1] << 16));
+    d[32 + p] = (int32_t)((uint32_t)tau[2 * p] | ((uint32_t)tau[2 * p + 1] << 16));
+    d[40 + p] = (int32_t)((uint32_t)dm[2 * p] | ((uint32_t)dm[2 * p + 1] << 16));
+  }
+}
+
+// Per solve, order of the panel records of each block: records whose slots
+// share one shift ("uniform", span 0) first, then the rest; within each
+// kind by descending cm = min(floor((P_i + emax) / C), cap - 1), the last
+// column whose cells the record's window reaches.  For every column x < cap
+// the live table holds, per kind, the number of records with cm >= x: a
+// prefix of the kind's records that contains every record whose window
+// reaches column x (for x = cap - 1 also columns beyond).  meta[4] = the
+// number of uniform records.
+__global__ __launch_bounds__(256) void k_rec_sort(int32_t C, int32_t cap, const int64_t* clu_ptr,
+                                                  const int32_t* src, int32_t* dst, int32_t* meta,
+                                                  int32_t* live) {
+  constexpr int kPer = 2 * kLiveCap / 256;       // bins per thread in the scan
+  __shared__ int32_t bin[2 * kLiveCap];
+  __shared__ int32_t s_part[256];
+  const int64_t b = blockIdx.x;
+  const int64_t base = clu_ptr[b];
+  const int32_t n = meta[b * kMetaInts + 0];
+  const int tid = threadIdx.x;
+  const int nb = 2 * cap;
+  for (int x = tid; x < 2 * kLiveCap; x += 256) bin[x] = 0;
+  __syncthreads();
+  auto key_of = [&](const int32_t* rec) {
+    const int32_t cm = min((rec[3] + rec[6]) / C, cap - 1);
+    return (rec[2] != 0 ? cap : 0) + (cap - 1 - cm);
+  };
+  for (int32_t r = tid; r < n; r += 256) atomicAdd(&bin[key_of(src + (base + r) * kRecInts)], 1);
+  __syncthreads();
+  // exclusive prefix over the 2 * cap bins (kPer consecutive bins per thread)
+  int32_t loc[kPer];
+  int32_t run = 0;
+  for (int x = 0; x < kPer; x++) {
+    const int k = tid * kPer + x;
+    loc[x] = run;
+    run += k < nb ? bin[k] : 0;
+  }
+  s_part[tid] = run;
+  __syncthreads();
+  if (tid == 0) {
+    int32_t acc = 0;
+    for (int q = 0; q < 256; q++) {
+      const int32_t v = s_part[q];
+      s_part[q] = acc;
+      acc += v;
+    }
+  }
+  __syncthreads();
+  for (int x = 0; x < kPer; x++) {
+    const int k = tid * kPer + x;
+    if (k < nb) bin[k] = s_part[tid] + loc[x];    // exclusive prefix P[k]
+  }
+  __syncthreads();
+  // live counts: kind s, column x -> P[s cap + cap - x] - P[s cap]
+  auto P = [&](int k) { return k < nb ? bin[k] : n; };
+  for (int x = tid; x < cap; x += 256) {
+    live[((int64_t)b * cap + x) * 2 + 0] = P(cap - x) - P(0);
+    live[((int64_t)b * cap + x) * 2 + 1] = P(2 * cap - x) - P(cap);
+  }
+  if (tid == 0) meta[b * kMetaInts + 4] = P(cap);
+  __syncthreads();
+  // scatter (bins become cursors)
+  for (int32_t r = tid; r < n; r += 256) {
+    const int32_t* rec = src + (base + r) * kRecInts;
+    const int32_t pos = atomicAdd(&bin[key_of(rec)], 1);
+    int32_t* d = dst + (base + pos) * kRecInts;
+    for (int x = 0; x < kRecInts; x++) d[x] = rec[x];
+  }
+}
+
+// Every table cell after row 0 starts out as "not written yet".
+__global__ void k_fill_pending(uint4* p, int64_t n16) {
+  const uint32_t v = kPendM | (kPendM << 16);
+  for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < n16;
+       x += (int64_t)gridDim.x * blockDim.x)
+    p[x] = make_uint4(v, v, v, v);
+}
+
+// Left padding of every row (cells of its 64-cell-aligned slot before the
+// row) and an 8-cell sentinel hold infinity, so that 16-byte window loads
+// that touch them read infinity.
+__global__ void k_pad_init(int64_t F, const int32_t* w, const int64_t* row_off, uint16_t* m,
+                           uint16_t* sentinel) {
+  for (int64_t s = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; s < F;
+       s += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t pad = ((int64_t)w[s] + kRowAlign - 1) / kRowAlign * kRowAlign;
+    const int64_t start = row_off[s] + w[s] - pad;
+    for (int64_t x = start; x < row_off[s]; x++) m[x] = (uint16_t)kInfM;
+  }
+  if (blockIdx.x == 0 && threadIdx.x < 8) sentinel[threadIdx.x] = (uint16_t)kInfM;
+}
+
+}  // namespace
+
+hipError_t launch_rec_prepare(rc_solution sol, hipStream_t s) {
+  rc_family f = sol->f;
+  hipLaunchKernelGGL(k_rec_prepare, dim3((unsigned)f->nblk), dim3(256), 0, s, f->F,
+                     (int32_t)sol->Beff, f->w, f->row_off, f->rec_ptr, f->clu_ptr, f->rec,
+                     sol->crec_tmp, sol->blk_meta);
+  return hipGetLastError();
+}
+
+hipError_t launch_rec_sort(rc_solution sol, int32_t C, hipStream_t s) {
+  rc_family f = sol->f;
+  hipLaunchKernelGGL(k_rec_sort, dim3((unsigned)f->nblk), dim3(256), 0, s, C, sol->live_cap,
+                     f->clu_ptr, sol->crec_tmp, sol->crec, sol->blk_meta, sol->live);
+  return hipGetLastError();
+}
+
+hipError_t launch_push_prepare(rc_solution sol, int32_t C, hipStream_t s) {
+  rc_family f = sol->f;
+  hipLaunchKernelGGL(k_push_prepare, dim3((unsigned)f->nblk), dim3(64), 0, s, f->F, f->nblk,
+                     (int32_t)sol->Beff, C, f->w, f->row_off, f->rec_ptr, f->rec, sol->push);
+  return hipGetLastError();
+}
+
+// Cells [64, cells) (row 0 is the first row and fills one 64-cell line).
+hipError_t launch_fill_pending(rc_solution sol, hipStream_t s) {
+  rc_family f = sol->f;
+  const int64_t n16 = (f->cells - kRowAlign) / 8;
+  if (n16 <= 0) return hipSuccess;
+  const unsigned grid = (unsigned)std::min<int64_t>((n16 + 255) / 256, 4096);
+  hipLaunchKernelGGL(k_fill_pending, dim3(grid), dim3(256), 0, s,
+                     reinterpret_cast<uint4*>(sol->m + kRowAlign), n16);
+  return hipGetLastError();
+}
+
+hipError_t launch_blk_clusters(rc_family f, int64_t* count, hipStream_t s) {
+  hipLaunchKernelGGL(k_blk_clusters, dim3((unsigned)f->nblk), dim3(256), 0, s, f->rec_ptr, f->rec,
+                     count);
+  return hipGetLastError();
+}
+
+hipError_t launch_pad_init(rc_solution sol, hipStream_t s) {
+  rc_family f = sol->f;
+  const unsigned grid = (unsigned)std::min<int64_t>((f->F + 255) / 256, 1024);
+  hipLaunchKernelGGL(k_pad_init, dim3(grid > 0 ? grid : 1), dim3(256), 0, s, f->F, f->w,
+                     f->row_off, sol->m, sol->sentinel);
   return hipGetLastError();
 }
 

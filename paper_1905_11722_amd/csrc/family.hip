@@ -64,20 +64,37 @@ __global__ void k_graph_masks(int n, int words, const int32_t* row_ptr, const in
 // workgroup; the closure lives in LDS when it fits.
 template <bool kLds>
 __global__ __launch_bounds__(1024) void k_ancestors(int n, int words, int num_depths,
-                                                    const int32_t* by_depth,
+                                                    int num_edges, const int32_t* by_depth,
                                                     const int32_t* depth_ptr,
                                                     const int32_t* pred_ptr,
                                                     const int32_t* pred_idx, uint64_t* anc_out) {
+  // LDS variant: the ancestor masks, the depth order and the predecessor
+  // lists all live in LDS, so each depth costs LDS traffic and one barrier
   extern __shared__ uint64_t lds_anc[];
   uint64_t* anc = kLds ? lds_anc : anc_out;
+  int32_t* l_pp = reinterpret_cast<int32_t*>(lds_anc + (kLds ? (int64_t)n * words : 0));
+  int32_t* l_pi = l_pp + (n + 1);
+  int32_t* l_bd = l_pi + num_edges;
+  int32_t* l_dp = l_bd + n;
+  if (kLds) {
+    for (int x = threadIdx.x; x <= n; x += blockDim.x) l_pp[x] = pred_ptr[x];
+    for (int x = threadIdx.x; x < num_edges; x += blockDim.x) l_pi[x] = pred_idx[x];
+    for (int x = threadIdx.x; x < n; x += blockDim.x) l_bd[x] = by_depth[x];
+    for (int x = threadIdx.x; x <= num_depths; x += blockDim.x) l_dp[x] = depth_ptr[x];
+    __syncthreads();
+  }
+  const int32_t* PP = kLds ? l_pp : pred_ptr;
+  const int32_t* PI = kLds ? l_pi : pred_idx;
+  const int32_t* BD = kLds ? l_bd : by_depth;
+  const int32_t* DP = kLds ? l_dp : depth_ptr;
   for (int d = 0; d < num_depths; d++) {
-    const int b = depth_ptr[d], e = depth_ptr[d + 1];
+    const int b = DP[d], e = DP[d + 1];
     const int items = (e - b) * words;
     for (int it = threadIdx.x; it < items; it += blockDim.x) {
-      const int v = by_depth[b + it / words];
+      const int v = BD[b + it / words];
       const int w = it % words;
       uint64_t x = (v >> 6) == w ? (1ull << (v & 63)) : 0ull;
-      for (int q = pred_ptr[v]; q < pred_ptr[v + 1]; q++) x |= anc[(int64_t)pred_idx[q] * words + w];
+      for (int q = PP[v]; q < PP[v + 1]; q++) x |= anc[(int64_t)PI[q] * words + w];
       anc[(int64_t)v * words + w] = x;
     }
     __syncthreads();
@@ -193,50 +210,64 @@ __device__ __forceinline__ int popcnt_set(const uint64_t* a, int words) {
   return c;
 }
 
-// Canonical order: ascending size, then ascending numeric value.
-// Exact family: candidates are grouped by size level (reverse search
-// yields no duplicates) and ranked within their level.  Pruned family:
-// candidates are [0] the empty set, [1..n] the sets L^v (pairwise distinct),
-// [n+1] V; V is dropped when some L^v already equals V.  Output is
-// word-major: bits[w * fstride + index].
-__global__ __launch_bounds__(256) void k_rank(int words, int mode, int n, const uint64_t* cand,
+// Canonical order: ascending size, then ascending numeric value.  Exact
+// family: candidates are grouped by size level (reverse search yields no
+// duplicates) and ranked within their level.  Output is word-major:
+// bits[w * fstride + index].
+__global__ __launch_bounds__(256) void k_rank(int words, int n, const uint64_t* cand,
                                               const int32_t* lvl, uint64_t* bits, int64_t fstride,
                                               DevStatus* st) {
   const int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-  const uint64_t* X;
-  int64_t rank;
-  if (mode == RC_FAMILY_EXACT) {
-    const int64_t total = lvl[n + 1];
-    if (x >= total) return;
-    X = cand + x * words;
-    const int s = popcnt_set(X, words);
-    rank = lvl[s];
-    for (int64_t y = lvl[s]; y < lvl[s + 1]; y++)
-      if (y != x && cmp_value(cand + y * words, X, words) < 0) rank++;
-    if (x == 0) st->count = st->overflow ? st->count : total;
-  } else {
-    const int64_t total = (int64_t)n + 2;
-    if (x >= total) return;
-    bool vdup = n == 0;                    // V is the empty set itself
-    for (int64_t y = 1; y <= n && !vdup; y++) vdup = popcnt_set(cand + y * words, words) == n;
-    if (vdup && x == n + 1) return;
-    const int64_t valid = vdup ? n + 1 : n + 2;
-    X = cand + x * words;
-    const int sx = popcnt_set(X, words);
-    rank = 0;
-    for (int64_t y = 0; y < valid; y++) {
-      if (y == x) continue;
-      const uint64_t* Y = cand + y * words;
-      const int sy = popcnt_set(Y, words);
-      if (sy < sx || (sy == sx && cmp_value(Y, X, words) < 0)) rank++;
-    }
-    if (x == 0) st->count = valid;
-  }
+  const int64_t total = lvl[n + 1];
+  if (x >= total) return;
+  const uint64_t* X = cand + x * words;
+  const int s = popcnt_set(X, words);
+  int64_t rank = lvl[s];
+  for (int64_t y = lvl[s]; y < lvl[s + 1]; y++)
+    if (y != x && cmp_value(cand + y * words, X, words) < 0) rank++;
+  if (x == 0) st->count = st->overflow ? st->count : total;
   if (rank >= fstride) {
     st->error = 1;
     return;
   }
   for (int w = 0; w < words; w++) bits[(int64_t)w * fstride + rank] = X[w];
+}
+
+// Pruned family: candidates are [0] the empty set, [1..n] the sets L^v
+// (pairwise distinct), [n+1] V, which is dropped when some L^v already
+// equals V.  One workgroup: candidate sizes in LDS, then every candidate
+// counts the candidates before it (smaller size, or equal size and smaller
+// numeric value).
+__global__ __launch_bounds__(1024) void k_rank_pruned(int words, int n, const uint64_t* cand,
+                                                      uint64_t* bits, int64_t fstride,
+                                                      DevStatus* st) {
+  __shared__ int32_t s_sz[kMaxNodes + 2];
+  __shared__ int32_t s_vdup;
+  const int64_t total = (int64_t)n + 2;
+  if (threadIdx.x == 0) s_vdup = n == 0;             // V is the empty set itself
+  __syncthreads();
+  for (int64_t x = threadIdx.x; x < total; x += blockDim.x)
+    s_sz[x] = popcnt_set(cand + x * words, words);
+  __syncthreads();
+  for (int64_t x = 1 + threadIdx.x; x <= n; x += blockDim.x)
+    if (s_sz[x] == n) s_vdup = 1;                     // some L^v is V already
+  __syncthreads();
+  const int64_t valid = s_vdup ? n + 1 : n + 2;
+  for (int64_t x = threadIdx.x; x < valid; x += blockDim.x) {
+    const uint64_t* X = cand + x * words;
+    const int sx = s_sz[x];
+    int64_t rank = 0;
+    for (int64_t y = 0; y < valid; y++) {
+      const int sy = s_sz[y];
+      if (y != x && (sy < sx || (sy == sx && cmp_value(cand + y * words, X, words) < 0))) rank++;
+    }
+    if (rank >= fstride) {
+      st->error = 1;
+      continue;
+    }
+    for (int w = 0; w < words; w++) bits[(int64_t)w * fstride + rank] = X[w];
+  }
+  if (threadIdx.x == 0) st->count = valid;
 }
 
 // ------------------------------------------------------- per-set values
@@ -465,13 +496,17 @@ hipError_t launch_graph_masks(rc_graph g, const int32_t* d_row_ptr, const int32_
 }
 
 hipError_t launch_ancestors(rc_graph g, uint64_t* anc, hipStream_t s) {
-  const size_t lds = sizeof(uint64_t) * (size_t)g->n * g->words;
-  if (lds <= 48 * 1024) {
+  const size_t lds = sizeof(uint64_t) * (size_t)g->n * g->words +
+                     sizeof(int32_t) * ((size_t)g->n + 1 + g->num_pred_edges + g->n +
+                                        g->num_depths + 1);
+  if (lds <= 64 * 1024) {
     hipLaunchKernelGGL(k_ancestors<true>, dim3(1), dim3(1024), lds, s, g->n, g->words,
-                       g->num_depths, g->dByDepth, g->dDepthPtr, g->dPredPtr, g->dPredIdx, anc);
+                       g->num_depths, g->num_pred_edges, g->dByDepth, g->dDepthPtr, g->dPredPtr,
+                       g->dPredIdx, anc);
   } else {
     hipLaunchKernelGGL(k_ancestors<false>, dim3(1), dim3(1024), 0, s, g->n, g->words,
-                       g->num_depths, g->dByDepth, g->dDepthPtr, g->dPredPtr, g->dPredIdx, anc);
+                       g->num_depths, g->num_pred_edges, g->dByDepth, g->dDepthPtr, g->dPredPtr,
+                       g->dPredIdx, anc);
   }
   return hipGetLastError();
 }
@@ -496,8 +531,13 @@ hipError_t launch_enum_exact(rc_graph g, uint64_t* cand, int64_t cap, int32_t* l
 hipError_t launch_rank(rc_graph g, int32_t mode, const uint64_t* cand, int64_t ncand_max,
                        const int32_t* lvl, uint64_t* bits, int64_t fstride, DevStatus* st,
                        hipStream_t s) {
-  hipLaunchKernelGGL(k_rank, dim3((unsigned)((ncand_max + 255) / 256)), dim3(256), 0, s, g->words,
-                     mode, g->n, cand, lvl, bits, fstride, st);
+  if (mode == RC_FAMILY_PRUNED) {
+    hipLaunchKernelGGL(k_rank_pruned, dim3(1), dim3(1024), 0, s, g->words, g->n, cand, bits,
+                       fstride, st);
+  } else {
+    hipLaunchKernelGGL(k_rank, dim3((unsigned)((ncand_max + 255) / 256)), dim3(256), 0, s,
+                       g->words, g->n, cand, lvl, bits, fstride, st);
+  }
   return hipGetLastError();
 }
 

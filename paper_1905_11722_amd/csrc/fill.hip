@@ -5,17 +5,19 @@
 // Table layout: one row per family member L, holding the cells
 // t = 0 .. w_L - 1 (w_L = T(L \ boundary(L)) + 1; every cell beyond is
 // provably infinite, since each recomputed node of a chain ending at L lies
-// in L \ boundary(L)).  Rows are contiguous in t and start on 128-byte lines.
-// A cell stores m = opt[L, t] as uint16 (0xFFFF = infinity) and optarg as the
-// uint16 family index of the predecessor.
+// in L \ boundary(L)).  Rows are contiguous in t and end on 128-byte
+// lines.  A cell stores m = opt[L, t] as uint16 (0xFFFF = infinity).
 //
 // Pull form of Algorithm 1: opt[L', t'] is the minimum over predecessors
 // L (proper subsets of L' in the family) of opt[L, t' - dt] + dm, taken
-// over the sources that pass the budget test opt[L, t] + c <= B.  The
-// strict update of Algorithm 1, which visits sources in ascending family
-// index, keeps the first (smallest-index) source among equal minima; the
-// kernel reproduces that with one unsigned minimum over the packed key
-// (m' << 16) | index(L).
+// over the sources that pass the budget test opt[L, t] + c <= B.
+//
+// optarg is not stored by the fill.  Algorithm 1's strict update over
+// ascending sources makes optarg[L', t'] the smallest family index L among
+// the predecessors whose cell passes the budget test and reproduces
+// opt[L', t'] (the first source to reach the minimum writes it, later ones
+// only tie).  That rule is evaluated where optarg is needed: at every step
+// of the traceback (k_trace) and, for a whole-table export, by k_arg_all.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -46,11 +48,10 @@ __device__ __forceinline__ int64_t word_cost(uint64_t bits, int word, const int3
 }
 
 // opt[empty, 0] = 0 (Algorithm 1's initial condition); selection state.
-__global__ void k_solve_init(uint16_t* m, uint16_t* arg, const int64_t* row_off, int objective,
+__global__ void k_solve_init(uint16_t* m, const int64_t* row_off, int objective,
                              DevStatus* st) {
   if (threadIdx.x == 0) {
     m[row_off[0]] = 0;
-    arg[row_off[0]] = (uint16_t)kNoArg;
     st->error = 0;
     st->t_sel = objective == RC_TIME_CENTRIC ? INT32_MAX : -1;
     st->m_sel = -1;
@@ -66,15 +67,14 @@ __global__ __launch_bounds__(kFillThreads) void k_fill_level(
     int64_t lb, const int32_t* __restrict__ w, const int64_t* __restrict__ row_off,
     const int64_t* __restrict__ pred_ptr, const int32_t* __restrict__ pidx,
     const int32_t* __restrict__ pdt, const int32_t* __restrict__ pdm,
-    const int32_t* __restrict__ pc, int32_t Beff, uint16_t* __restrict__ m,
-    uint16_t* __restrict__ arg) {
+    const int32_t* __restrict__ pc, int32_t Beff, uint16_t* __restrict__ m) {
   const int64_t j = lb + blockIdx.y;
   const int32_t wj = w[j];
   const int32_t tile0 = blockIdx.x * kTile;
   if (tile0 >= wj) return;
   uint32_t acc[kCellsPerThread];
 #pragma unroll
-  for (int r = 0; r < kCellsPerThread; r++) acc[r] = 0xFFFFFFFFu;
+  for (int r = 0; r < kCellsPerThread; r++) acc[r] = kInfM;
   const int64_t p0 = pred_ptr[j], p1 = pred_ptr[j + 1];
   for (int64_t p = p0; p < p1; ++p) {
     // budget test of Algorithm 1: opt[L, t] + c <= B, i.e. opt[L, t] <= tau
@@ -85,26 +85,52 @@ __global__ __launch_bounds__(kFillThreads) void k_fill_level(
     const int32_t wi = w[i];
     if (dt >= tile0 + kTile || dt + wi <= tile0) continue;  // window misses the tile
     const uint16_t* src = m + row_off[i];
-    const uint32_t kadd = ((uint32_t)pdm[p] << 16) | (uint32_t)i;
+    const uint32_t dm = (uint32_t)pdm[p];
 #pragma unroll
     for (int r = 0; r < kCellsPerThread; r++) {
       const int32_t t = tile0 + r * kFillThreads + (int32_t)threadIdx.x - dt;
       if ((uint32_t)t < (uint32_t)wi) {
         const uint32_t x = src[t];
-        if (x <= (uint32_t)tau) acc[r] = min(acc[r], (x << 16) + kadd);
+        if (x <= (uint32_t)tau) acc[r] = min(acc[r], x + dm);
       }
     }
   }
   uint16_t* mo = m + row_off[j];
-  uint16_t* ao = arg + row_off[j];
 #pragma unroll
   for (int r = 0; r < kCellsPerThread; r++) {
     const int32_t tp = tile0 + r * kFillThreads + (int32_t)threadIdx.x;
-    if (tp < wj) {
-      mo[tp] = (uint16_t)(acc[r] >> 16);
-      ao[tp] = (uint16_t)(acc[r] & 0xFFFFu);
+    if (tp < wj) mo[tp] = (uint16_t)acc[r];
+  }
+}
+
+// optarg of every cell of targets [lb, lb + gridDim.y) from the final
+// table: the smallest predecessor index whose cell passes the budget test
+// and reproduces the target value (Algorithm 1's first writer).
+__global__ __launch_bounds__(kFillThreads) void k_arg_all(
+    int64_t lb, const int32_t* __restrict__ w, const int64_t* __restrict__ row_off,
+    const int64_t* __restrict__ pred_ptr, const int32_t* __restrict__ pidx,
+    const int32_t* __restrict__ pdt, const int32_t* __restrict__ pdm,
+    const int32_t* __restrict__ pc, int32_t Beff, const uint16_t* __restrict__ m,
+    uint16_t* __restrict__ arg) {
+  const int64_t j = lb + blockIdx.y;
+  const int32_t wj = w[j];
+  const int32_t tp = blockIdx.x * kFillThreads + threadIdx.x;
+  if (tp >= wj) return;
+  const uint32_t mj = m[row_off[j] + tp];
+  uint32_t a = kNoArg;
+  if (mj != kInfM && j > 0) {
+    for (int64_t p = pred_ptr[j]; p < pred_ptr[j + 1]; ++p) {
+      const int32_t t = tp - pdt[p];
+      const int32_t i = pidx[p];
+      if ((uint32_t)t >= (uint32_t)w[i]) continue;
+      const int32_t x = m[row_off[i] + t];
+      if (x <= Beff - pc[p] && (uint32_t)(x + pdm[p]) == mj) {
+        a = (uint32_t)i;
+        break;
+      }
     }
   }
+  arg[row_off[j] + tp] = (uint16_t)a;
 }
 
 // t* = min (time-centric) or max (memory-centric) finite t of row V.
@@ -129,79 +155,158 @@ __global__ void k_select_finish(const uint16_t* m, const int64_t* row_off, int64
   st->m_sel = st->t_sel >= 0 ? (int32_t)m[row_off[v] + st->t_sel] : -1;
 }
 
-// Traceback of optarg from (V, t*) (Section 4.2), then Eq. 1 and Eq. 2 of
-// the chain from their definitions: U_i is the union of boundaries of
-// L_1..L_i, segment i needs M(U_{i-1}) + 2 M(V_i) + A(L_i), the overhead is
-// T(V \ U_k).  One wave; lane w holds word w of the sets.
-__global__ __launch_bounds__(kWave) void k_trace(
+// Traceback from (V, t*) (Section 4.2), then Eq. 1 and Eq. 2 of the chain
+// from their definitions: U_i is the union of boundaries of L_1..L_i,
+// segment i needs M(U_{i-1}) + 2 M(V_i) + A(L_i), the overhead is
+// T(V \ U_k).  At each step the workgroup scans the predecessors of L'
+// (ascending family index, kTraceThreads at a time) for optarg[L', t']:
+// the smallest index whose cell passes the budget test and reproduces the
+// target value.  The re-evaluation runs on wave 0, lane w holding word w.
+constexpr int kTraceThreads = 256;
+constexpr int kTraceLds = 2048;       // families up to this size keep their per-set arrays in LDS
+
+__global__ __launch_bounds__(kTraceThreads) void k_trace(
     int64_t F, int n, int words, int64_t fstride, const uint64_t* __restrict__ bits,
-    const uint64_t* __restrict__ bd, const int32_t* __restrict__ Tsum,
-    const int32_t* __restrict__ Msum, const int32_t* __restrict__ Tbd,
-    const int32_t* __restrict__ A, const int32_t* __restrict__ T, const int32_t* __restrict__ M,
-    const int32_t* __restrict__ w, const int64_t* __restrict__ row_off,
-    const uint16_t* __restrict__ arg, int64_t T_total, DevStatus* st, int32_t* chain,
-    int32_t* seg, uint8_t* cached) {
-  const int lane = threadIdx.x;
-  const bool active = lane < words;
+    const uint64_t* __restrict__ bd, const int32_t* __restrict__ A, const int32_t* __restrict__ T,
+    const int32_t* __restrict__ M, const int32_t* __restrict__ w,
+    const int64_t* __restrict__ row_off, const int64_t* __restrict__ pred_ptr,
+    const int32_t* __restrict__ pidx, const int32_t* __restrict__ pdt,
+    const int32_t* __restrict__ pdm, const int32_t* __restrict__ pc, int32_t Beff,
+    const uint16_t* __restrict__ m, int64_t T_total, DevStatus* st, int32_t* chain, int32_t* seg,
+    uint8_t* cached) {
+  // per-set arrays of small families live in LDS for the whole walk
+  __shared__ int32_t s_w[kTraceLds];
+  __shared__ int64_t s_off[kTraceLds];
+  __shared__ int64_t s_pp[kTraceLds + 1];
+  // per chunk of predecessors, alternating by parity: the first hit of each
+  // wave and every thread's (source, dt)
+  __shared__ int32_t s_first[2][kTraceThreads / kWave];
+  __shared__ int32_t s_src[2][kTraceThreads];
+  __shared__ int32_t s_dt[2][kTraceThreads];
+  __shared__ int32_t s_chain[kMaxNodes + 1];        // a chain adds a node per step
+  __shared__ int32_t s_M[kMaxNodes];
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1), wave = tid / kWave;
+  const bool in_lds = F <= kTraceLds;
+  if (in_lds) {
+    for (int64_t x = tid; x < F; x += kTraceThreads) {
+      s_w[x] = w[x];
+      s_off[x] = row_off[x];
+      s_pp[x] = pred_ptr[x];
+    }
+    if (tid == 0) s_pp[F] = pred_ptr[F];
+  }
+  __syncthreads();
+  auto Wd = [&](int64_t i) { return in_lds ? s_w[i] : w[i]; };
+  auto Off = [&](int64_t i) { return in_lds ? s_off[i] : row_off[i]; };
+  auto PP = [&](int64_t i) { return in_lds ? s_pp[i] : pred_ptr[i]; };
+
+  // The walk is identical in every thread; only the predecessor scan is split.
   int64_t j = F - 1;
   int64_t t = st->t_sel;
   int32_t k = 0;
   bool bad = t < 0;
+  int par = 0;
   while (j != 0 && !bad) {
-    if (t < 0 || t >= w[j]) {
+    if (t < 0 || t >= Wd(j) || k >= F || k > n) {     // each step removes a node
       bad = true;
       break;
     }
-    const uint32_t a = arg[row_off[j] + t];
-    if (a == kNoArg || a >= (uint32_t)j || k >= F) {
+    const uint32_t mj = m[Off(j) + t];
+    const int64_t p0 = PP(j), p1 = PP(j + 1);
+    int32_t next_i = -1, next_dt = 0;
+    for (int64_t base = p0; base < p1 && next_i < 0; base += kTraceThreads) {
+      const int64_t p = base + tid;
+      bool hit = false;
+      int32_t i = 0, dt = 0;
+      if (p < p1) {
+        i = pidx[p];
+        dt = pdt[p];
+        const int32_t c = pc[p], dm = pdm[p];
+        const int64_t ts = t - dt;
+        if (ts >= 0 && ts < Wd(i)) {
+          const int32_t x = m[Off(i) + ts];
+          hit = x <= Beff - c && (uint32_t)(x + dm) == mj;
+        }
+      }
+      const unsigned long long bal = __ballot(hit);
+      if (lane == 0) s_first[par][wave] = bal ? wave * kWave + __ffsll((long long)bal) - 1 : INT32_MAX;
+      s_src[par][tid] = i;
+      s_dt[par][tid] = dt;
+      __syncthreads();
+      int32_t f = INT32_MAX;
+#pragma unroll
+      for (int q = 0; q < kTraceThreads / kWave; q++) f = min(f, s_first[par][q]);
+      if (f != INT32_MAX) {                    // the smallest predecessor index that hits
+        next_i = s_src[par][f];
+        next_dt = s_dt[par][f];
+      }
+      par ^= 1;
+    }
+    if (next_i < 0 || mj == kInfM) {
       bad = true;
       break;
     }
-    const int64_t i = a;
-    const uint64_t x = active ? bits[(int64_t)lane * fstride + i] & bd[(int64_t)lane * fstride + j] : 0ull;
-    const int64_t ti = wave_sum_i64(active ? word_cost(x, lane, T) : 0);
-    t -= (int64_t)Tsum[j] - Tbd[j] - Tsum[i] + ti;   // T((L_j \ L_i) \ bd(L_j))
-    if (lane == 0) chain[k] = (int32_t)j;
+    if (tid == 0) chain[k] = (int32_t)j;
     k++;
-    j = i;
+    t -= next_dt;
+    j = next_i;
   }
-  if (t != 0) bad = true;                             // the walk must end at (empty, 0)
+  if (t != 0) bad = true;                            // the walk must end at (empty, 0)
+  __syncthreads();
   if (bad) {
-    if (lane == 0) {
+    if (tid == 0) {
       st->error = 2;
       st->k = -1;
     }
     return;
   }
-  __syncthreads();
-  for (int c = lane; c < k / 2; c += kWave) {         // chain in increasing order
-    const int32_t tmp = chain[c];
-    chain[c] = chain[k - 1 - c];
-    chain[k - 1 - c] = tmp;
+  // chain in increasing order, kept in LDS as well; node memories in LDS
+  for (int c = tid; c < k; c += kTraceThreads) s_chain[c] = chain[k - 1 - c];
+  for (int v = tid; v < n; v += kTraceThreads) {
+    seg[v] = -1;
+    s_M[v] = M[v];
   }
   __syncthreads();
-  for (int v = lane; v < n; v += kWave) seg[v] = -1;
-  __syncthreads();
+  for (int c = tid; c < k; c += kTraceThreads) chain[c] = s_chain[c];
+  if (tid >= kWave) return;
+  // Eq. 2 per segment: M(U_{i-1}) + 2 M(V_i) + A(L_i), U grows by the
+  // boundary of each L_i; the loads of kPre chain steps are issued together
+  constexpr int kPre = 4;
+  const bool active = lane < words;
   uint64_t U = 0, prev = 0;
-  int64_t peak = 0;
-  for (int c = 0; c < k; c++) {
-    const int64_t s = chain[c];
-    const uint64_t L = active ? bits[(int64_t)lane * fstride + s] : 0ull;
-    const uint64_t Vi = L & ~prev;
-    const int64_t mu = wave_sum_i64(active ? word_cost(U, lane, M) : 0);
-    const int64_t mv = wave_sum_i64(active ? word_cost(Vi, lane, M) : 0);
-    const int64_t mem = mu + 2 * mv + A[s];
-    peak = mem > peak ? mem : peak;
-    for (uint64_t b = Vi; b; b &= b - 1) seg[lane * 64 + __builtin_ctzll(b)] = c;
-    if (active) U |= bd[(int64_t)lane * fstride + s];
-    prev = L;
+  int64_t mu = 0, peak = 0;
+  for (int c0 = 0; c0 < k; c0 += kPre) {
+    uint64_t Ls[kPre], Bs[kPre];
+    int32_t As[kPre];
+#pragma unroll
+    for (int x = 0; x < kPre; x++) {
+      const int c = c0 + x < k ? c0 + x : k - 1;
+      const int64_t sx = s_chain[c];
+      Ls[x] = active ? bits[(int64_t)lane * fstride + sx] : 0ull;
+      Bs[x] = active ? bd[(int64_t)lane * fstride + sx] : 0ull;
+      As[x] = A[sx];
+    }
+#pragma unroll
+    for (int x = 0; x < kPre; x++) {
+      const int c = c0 + x;
+      if (c >= k) break;
+      const uint64_t Vi = Ls[x] & ~prev;
+      const int64_t mv = wave_sum_i64(active ? word_cost(Vi, lane, s_M) : 0);
+      const int64_t mem = mu + 2 * mv + As[x];
+      peak = mem > peak ? mem : peak;
+      for (uint64_t bb = Vi; bb; bb &= bb - 1) seg[lane * 64 + __builtin_ctzll(bb)] = c;
+      const uint64_t add = Bs[x] & ~U;
+      mu += wave_sum_i64(active ? word_cost(add, lane, s_M) : 0);
+      U |= add;
+      prev = Ls[x];
+    }
   }
   for (int b = 0; b < 64 && active; b++) {
     const int v = lane * 64 + b;
     if (v < n) cached[v] = (uint8_t)((U >> b) & 1ull);
   }
   const int64_t tu = wave_sum_i64(active ? word_cost(U, lane, T) : 0);
-  const int64_t mu = wave_sum_i64(active ? word_cost(U, lane, M) : 0);
   if (lane == 0) {
     st->k = k;
     st->overhead = T_total - tu;
@@ -214,7 +319,7 @@ __global__ __launch_bounds__(kWave) void k_trace(
 
 hipError_t launch_solve_init(rc_solution sol, hipStream_t s) {
   rc_family f = sol->f;
-  hipLaunchKernelGGL(k_solve_init, dim3(1), dim3(64), 0, s, sol->m, sol->arg, f->row_off,
+  hipLaunchKernelGGL(k_solve_init, dim3(1), dim3(64), 0, s, sol->m, f->row_off,
                      sol->objective, sol->status);
   return hipGetLastError();
 }
@@ -228,7 +333,7 @@ hipError_t launch_fill(rc_solution sol, hipStream_t s) {
     if (tiles <= 0 || le <= lb) continue;
     hipLaunchKernelGGL(k_fill_level, dim3((unsigned)tiles, (unsigned)(le - lb)),
                        dim3(kFillThreads), 0, s, lb, f->w, f->row_off, f->pred_ptr, f->pidx,
-                       f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, sol->m, sol->arg);
+                       f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, sol->m);
   }
   return hipGetLastError();
 }
@@ -248,9 +353,24 @@ hipError_t launch_select(rc_solution sol, hipStream_t s) {
 hipError_t launch_trace(rc_solution sol, hipStream_t s) {
   rc_family f = sol->f;
   rc_graph g = f->g;
-  hipLaunchKernelGGL(k_trace, dim3(1), dim3(kWave), 0, s, f->F, g->n, g->words, f->fstride,
-                     f->bits, f->bd, f->Tsum, f->Msum, f->Tbd, f->A, g->dT, g->dM, f->w,
-                     f->row_off, sol->arg, g->T_total, sol->status, sol->chain, sol->seg, sol->cached);
+  hipLaunchKernelGGL(k_trace, dim3(1), dim3(kTraceThreads), 0, s, f->F, g->n, g->words,
+                     f->fstride, f->bits, f->bd, f->A, g->dT, g->dM, f->w, f->row_off,
+                     f->pred_ptr, f->pidx, f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, sol->m,
+                     g->T_total, sol->status, sol->chain, sol->seg, sol->cached);
+  return hipGetLastError();
+}
+
+hipError_t launch_arg_all(rc_solution sol, hipStream_t s) {
+  rc_family f = sol->f;
+  const int64_t L = (int64_t)f->level_ptr.size() - 1;
+  for (int64_t l = 0; l < L; l++) {
+    const int64_t lb = f->level_ptr[l], le = f->level_ptr[l + 1];
+    const int64_t tiles = (f->level_maxw[l] + kFillThreads - 1) / kFillThreads;
+    if (tiles <= 0 || le <= lb) continue;
+    hipLaunchKernelGGL(k_arg_all, dim3((unsigned)tiles, (unsigned)(le - lb)), dim3(kFillThreads),
+                       0, s, lb, f->w, f->row_off, f->pred_ptr, f->pidx, f->pdt, f->pdm, f->pc,
+                       (int32_t)sol->Beff, sol->m, sol->arg);
+  }
   return hipGetLastError();
 }
 

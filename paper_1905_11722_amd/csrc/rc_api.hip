@@ -181,6 +181,7 @@ int rc_graph_create(int32_t n, const int32_t* row_ptr, const int32_t* col_idx, c
   if (st == RC_OK) st = upload(g->arena, T, n, &g->dT, s);
   if (st == RC_OK) st = upload(g->arena, M, n, &g->dM, s);
   if (st == RC_OK) st = upload(g->arena, pred_ptr.data(), n + 1, &g->dPredPtr, s);
+  g->num_pred_edges = (int32_t)pred_idx.size();
   if (st == RC_OK) st = upload(g->arena, pred_idx.data(), (int64_t)pred_idx.size(), &g->dPredIdx, s);
   if (st == RC_OK) st = upload(g->arena, by_depth.data(), n, &g->dByDepth, s);
   if (st == RC_OK) st = upload(g->arena, depth_ptr.data(), D + 1, &g->dDepthPtr, s);
@@ -328,20 +329,22 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
     BlockRecords& R = f->rec;
     const int64_t Rn = f->rec_total, T3 = f->nblk * kJB * kJB;
     R.src = A.get_n<int32_t>(Rn);
-    R.emin = A.get_n<int32_t>(Rn);
-    R.emax = A.get_n<int32_t>(Rn);
     R.e = A.get_n<int32_t>(Rn * kJB);
     R.kadd = A.get_n<uint32_t>(Rn * kJB);
     R.c = A.get_n<int32_t>(Rn * kJB);
     R.tri_e = A.get_n<int32_t>(T3);
     R.tri_kadd = A.get_n<uint32_t>(T3);
     R.tri_c = A.get_n<int32_t>(T3);
-    R.tri_emax = A.get_n<int32_t>(f->nblk * kJB);
-    R.blk_emax = A.get_n<int32_t>(f->nblk);
-    if (!R.src || !R.emin || !R.emax || !R.e || !R.kadd || !R.c || !R.tri_e || !R.tri_kadd ||
-        !R.tri_c || !R.tri_emax || !R.blk_emax)
+    if (!R.src || !R.e || !R.kadd || !R.c || !R.tri_e || !R.tri_kadd || !R.tri_c)
       return RC_E_NOMEM;
     RC_HIP(launch_blk_fill(f, f->nblk, s));
+    f->clu_ptr = A.get_n<int64_t>(f->nblk + 1);
+    if (!f->clu_ptr) return RC_E_NOMEM;
+    RC_HIP(launch_blk_clusters(f, counts, s));
+    RC_HIP(launch_scan(counts, f->clu_ptr, f->nblk, 1, s));
+    RC_HIP(hipMemcpyAsync(&f->clu_total, f->clu_ptr + f->nblk, sizeof(int64_t),
+                          hipMemcpyDeviceToHost, s));
+    RC_HIP(hipStreamSynchronize(s));
     f->has_records = true;
   }
   f->cells = f->row_off_host[F];
@@ -440,7 +443,7 @@ int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solutio
   if (!f || !out || B < 0) return RC_E_ARG;
   if (objective != RC_TIME_CENTRIC && objective != RC_MEMORY_CENTRIC) return RC_E_ARG;
   const int64_t Beff = std::min<int64_t>(B, 2 * f->g->M_total);
-  if (Beff > 0xFFFE) return RC_E_OVERFLOW;
+  if (Beff > kMaxBudget) return RC_E_OVERFLOW;
   hipStream_t s = as_stream(stream);
   rc_solution sol = new (std::nothrow) rc_solution_s();
   if (!sol) return RC_E_NOMEM;
@@ -460,12 +463,11 @@ int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solutio
     return st;
   };
   sol->m = sol->arena.get_n<uint16_t>(f->cells);
-  sol->arg = sol->arena.get_n<uint16_t>(f->cells);
   sol->status = sol->arena.get_n<DevStatus>(1);
   sol->chain = sol->arena.get_n<int32_t>(f->F);
   sol->seg = sol->arena.get_n<int32_t>(f->g->n);
   sol->cached = sol->arena.get_n<uint8_t>(f->g->n);
-  if (!sol->m || !sol->arg || !sol->status || !sol->chain || !sol->seg || !sol->cached)
+  if (!sol->m || !sol->status || !sol->chain || !sol->seg || !sol->cached)
     return fail(RC_E_NOMEM);
   if (hipEventCreate(&sol->ev0) != hipSuccess || hipEventCreate(&sol->ev1) != hipSuccess)
     return fail(RC_E_DEVICE);
@@ -473,7 +475,17 @@ int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solutio
   if (sol->fill_path == 1) {
     sol->progress = sol->arena.get_n<int32_t>(blocked_columns(f));
     sol->ticket = sol->arena.get_n<int32_t>(1);
-    if (!sol->progress || !sol->ticket) return fail(RC_E_NOMEM);
+    sol->crec = sol->arena.get_n<int32_t>(f->clu_total * kRecInts);
+    sol->crec_tmp = sol->arena.get_n<int32_t>(f->clu_total * kRecInts);
+    sol->live_cap = (int32_t)std::min<int64_t>(blocked_columns(f), kLiveCap);
+    sol->live = sol->arena.get_n<int32_t>(f->nblk * sol->live_cap * 2);
+    sol->blk_meta = sol->arena.get_n<int32_t>(f->nblk * kMetaInts);
+    sol->push = sol->arena.get_n<int32_t>(f->nblk * kJB * kPushInts);
+    sol->sentinel = sol->arena.get_n<uint16_t>(8);
+    if (!sol->progress || !sol->ticket || !sol->crec || !sol->crec_tmp || !sol->live ||
+        !sol->blk_meta ||
+        !sol->push || !sol->sentinel)
+      return fail(RC_E_NOMEM);
   }
   if (launch_solve_init(sol, s) != hipSuccess) return fail(RC_E_DEVICE);
   if (hipEventRecord(sol->ev0, s) != hipSuccess) return fail(RC_E_DEVICE);
@@ -553,11 +565,17 @@ int rc_export_table(rc_solution sol, int64_t first, int64_t count, int64_t* m_ho
   rc_family f = sol->f;
   hipStream_t s = as_stream(stream);
   const int64_t W = f->g->T_total + 1;
+  if (arg_host && !sol->arg) {               // optarg of the whole table, derived once
+    sol->arg = sol->arena.get_n<uint16_t>(f->cells);
+    if (!sol->arg) return RC_E_NOMEM;
+    RC_HIP(launch_arg_all(sol, s));
+  }
   const int64_t c0 = f->row_off_host[first], c1 = f->row_off_host[first + count];
-  std::vector<uint16_t> mm(c1 - c0), aa(c1 - c0);
+  std::vector<uint16_t> mm(c1 - c0), aa(arg_host ? c1 - c0 : 0);
   if (c1 > c0) {
     RC_HIP(hipMemcpyAsync(mm.data(), sol->m + c0, 2 * (c1 - c0), hipMemcpyDeviceToHost, s));
-    RC_HIP(hipMemcpyAsync(aa.data(), sol->arg + c0, 2 * (c1 - c0), hipMemcpyDeviceToHost, s));
+    if (arg_host)
+      RC_HIP(hipMemcpyAsync(aa.data(), sol->arg + c0, 2 * (c1 - c0), hipMemcpyDeviceToHost, s));
   }
   RC_HIP(hipStreamSynchronize(s));
   for (int64_t r = 0; r < count; r++) {
@@ -567,7 +585,7 @@ int rc_export_table(rc_solution sol, int64_t first, int64_t count, int64_t* m_ho
     for (int64_t t = 0; t < W; t++) {
       const bool in = t < w;
       const uint32_t mv = in ? mm[off + t] : kInfM;
-      const uint32_t av = in ? aa[off + t] : kNoArg;
+      const uint32_t av = (in && arg_host) ? aa[off + t] : kNoArg;
       if (m_host) m_host[r * W + t] = mv == kInfM ? -1 : (int64_t)mv;
       if (arg_host) arg_host[r * W + t] = (mv == kInfM || av == kNoArg) ? -1 : (int32_t)av;
     }

@@ -20,6 +20,16 @@ constexpr uint32_t kNoArg = 0xFFFFu;            // optarg = none
 constexpr int64_t kRowAlign = 64;               // cells; rows start on 128-byte lines
 constexpr int kJB = 8;                          // blocked fill: targets per block
 constexpr int64_t kMaxRecords = (int64_t)1 << 21;  // blocked fill: cap on panel records
+constexpr int kRecInts = 32;                    // blocked fill: int32 per compact record
+constexpr int kSpan = 248;                      // blocked fill: shifts staged together
+constexpr int kHalo = 512;                      // blocked fill: row pushes with shift <= kHalo
+                                                // read the row's halo, larger ones a window
+constexpr int kFarMax = 2 * kJB - 1;            // blocked fill: targets of one row's pushes
+constexpr int kPushInts = 64;                   // blocked fill: int32 per (block, row) push list
+constexpr int kMetaInts = 8;                    // blocked fill: int32 per block
+constexpr int kLiveCap = 2048;                  // blocked fill: columns with their own live counts
+constexpr uint32_t kPendM = 0xFFFE;             // blocked fill: cell not written yet
+constexpr int64_t kMaxBudget = 0xFFFC;          // finite opt values stay below kPendM
 
 // Device allocator with ownership tracking.
 struct Arena {
@@ -50,16 +60,12 @@ struct DevStatus {
 // Panel / triangle records of the blocked fill (blocks.hip).
 struct BlockRecords {
   int32_t* src = nullptr;       // [R] source family index
-  int32_t* emin = nullptr;      // [R] smallest shift among the record's slots
-  int32_t* emax = nullptr;      // [R] largest shift
   int32_t* e = nullptr;         // [R * kJB] shift of (src, j0 + slot), -1 = no pair
   uint32_t* kadd = nullptr;     // [R * kJB] (dm << 16) | src
   int32_t* c = nullptr;         // [R * kJB] budget term
   int32_t* tri_e = nullptr;     // [nblk * kJB * kJB] in-block pairs (row slot, target slot)
   uint32_t* tri_kadd = nullptr;
   int32_t* tri_c = nullptr;
-  int32_t* tri_emax = nullptr;  // [nblk * kJB] largest shift out of each in-block row, -1 none
-  int32_t* blk_emax = nullptr;  // [nblk] largest panel shift of the block
 };
 
 }  // namespace rcdp
@@ -75,6 +81,7 @@ struct rc_graph_s {
   uint64_t* dPred = nullptr;      // [n][words] predecessor masks
   int32_t* dPredPtr = nullptr;    // [n+1] predecessor CSR
   int32_t* dPredIdx = nullptr;
+  int32_t num_pred_edges = 0;
   int32_t* dByDepth = nullptr;    // nodes sorted by depth (longest path from a source)
   int32_t* dDepthPtr = nullptr;   // [num_depths+1]
   int32_t num_depths = 0;
@@ -101,6 +108,8 @@ struct rc_family_s {
   int64_t rec_total = 0;
   bool has_records = false;
   int64_t* rec_ptr = nullptr;     // [nblk+1]
+  int64_t* clu_ptr = nullptr;     // [nblk+1] compact records (shift clusters) per block
+  int64_t clu_total = 0;
   rcdp::BlockRecords rec;
   rcdp::DevStatus* status = nullptr;
   // host copies used for launches
@@ -118,13 +127,21 @@ struct rc_solution_s {
   int64_t t_star = -1, m_star = -1;
   rcdp::Arena arena;
   uint16_t* m = nullptr;          // [cells] opt values, kInfM = infinity
-  uint16_t* arg = nullptr;        // [cells] optarg family index, kNoArg = none
+  uint16_t* arg = nullptr;        // [cells] optarg, derived on demand by rc_export_table
   rcdp::DevStatus* status = nullptr;
   int32_t* chain = nullptr;       // [F]
   int32_t* seg = nullptr;         // [n]
   uint8_t* cached = nullptr;      // [n]
   int32_t* progress = nullptr;    // blocked fill: rows finished per column
   int32_t* ticket = nullptr;      // blocked fill: next column to take
+  int32_t* crec = nullptr;        // blocked fill: compact live records [clu_total * kRecInts]
+  int32_t* crec_tmp = nullptr;    // blocked fill: the same records before sorting
+  int32_t* live = nullptr;        // blocked fill: live records per (block, column, kind)
+  int32_t live_cap = 0;           // blocked fill: columns of the live table (min(K, kLiveCap))
+  int32_t* blk_meta = nullptr;    // blocked fill: per block metadata [nblk * kMetaInts]
+  int32_t* push = nullptr;        // blocked fill: row push lists [nblk * kJB * kPushInts]
+  int32_t cpt = 1;                // blocked fill: cells per thread of a column
+  uint16_t* sentinel = nullptr;   // 8 cells of infinity
   int32_t fill_path = 0;          // 0 level launches, 1 blocked wavefront
   hipEvent_t ev0 = nullptr, ev1 = nullptr;
   float fill_ms = 0.f;
@@ -165,11 +182,18 @@ hipError_t launch_solve_init(rc_solution sol, hipStream_t s);
 hipError_t launch_fill(rc_solution sol, hipStream_t s);
 hipError_t launch_select(rc_solution sol, hipStream_t s);
 hipError_t launch_trace(rc_solution sol, hipStream_t s);
+hipError_t launch_arg_all(rc_solution sol, hipStream_t s);
 
 // ---- blocked fill (blocks.hip, blocked.hip)
 hipError_t launch_row_align(rc_family f, hipStream_t s);
 hipError_t launch_blk_count(rc_family f, int64_t nblk, int64_t* count, hipStream_t s);
 hipError_t launch_blk_fill(rc_family f, int64_t nblk, hipStream_t s);
+hipError_t launch_blk_clusters(rc_family f, int64_t* count, hipStream_t s);
+hipError_t launch_rec_prepare(rc_solution sol, hipStream_t s);
+hipError_t launch_push_prepare(rc_solution sol, int32_t C, hipStream_t s);
+hipError_t launch_rec_sort(rc_solution sol, int32_t C, hipStream_t s);
+hipError_t launch_fill_pending(rc_solution sol, hipStream_t s);
+hipError_t launch_pad_init(rc_solution sol, hipStream_t s);
 int blocked_cells_per_thread(rc_family f);
 int64_t blocked_columns(rc_family f);
 hipError_t launch_fill_blocked(rc_solution sol, hipStream_t s);

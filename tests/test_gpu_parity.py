@@ -138,6 +138,12 @@ def test_budget_clamp_and_overflow(rc, oracle_mod):
     with pytest.raises(rc.RcError) as e:
         fb.solve(10 ** 6, "tc")
     assert e.value.status == rc.E_OVERFLOW
+    # the largest budget the 16-bit table takes, and one above it
+    small = W.Graph(2, [[1], []], [3, 4], [20000, 20000])
+    compare(rc, oracle_mod, small, "exact", 65532)
+    with pytest.raises(rc.RcError) as e:
+        rc.Graph.create(small).build_family("exact").solve(65533, "tc")
+    assert e.value.status == rc.E_OVERFLOW
     with pytest.raises(rc.RcError) as e:
         rc.Graph.create(W.antichain(12)).build_family("exact", max_sets=4095)
     assert e.value.status == rc.E_TOO_MANY_SETS
@@ -204,6 +210,19 @@ def test_fill_paths_small_cases(rc, oracle_mod, monkeypatch, path, name):
     g = c.graph
     for B in (c.B, 2 * max(g.M), sum(g.M), 2 * sum(g.M)):
         compare(rc, oracle_mod, g, c.mode, B)
+
+
+@pytest.mark.parametrize("cpt", ["1", "2", "4"])
+@pytest.mark.parametrize("n,p,seed", WIDE[::4])
+def test_wavefront_column_widths(rc, oracle_mod, monkeypatch, cpt, n, p, seed):
+    """The persistent fill at every column width (256, 512, 1024 cells)."""
+    monkeypatch.setenv("RCDP_FILL", "wavefront")
+    monkeypatch.setenv("RCDP_CPT", cpt)
+    g = W.random_dag(n, p, 7000 + seed, tmax=900, mmax=60)
+    lo, hi = 2 * max(g.M), 2 * sum(g.M)
+    for B in (lo, (lo + hi) // 2, hi):
+        for mode in ("exact", "pruned"):
+            compare(rc, oracle_mod, g, mode, B)
 
 
 @pytest.mark.parametrize("path", ["level", "wavefront"])
