@@ -186,6 +186,9 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);   // wave-uniform
   const int lane = tid & (kWave - 1);
   const bool ctl = wave == kCW;
+  // every step waits for the control wave's share of it while the compute
+  // waves keep the SIMDs busy: let the control wave issue first
+  if (ctl) __builtin_amdgcn_s_setprio(3);
   const u16x2 kInf2 = (u16x2)((unsigned short)kInfM);
   uint32_t step = 0;
   cint32* const meta = (cint32*)p.meta;
@@ -352,7 +355,19 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p) {
       poll_need = need;
       poll_t0 = wall_clock64();
     };
+    // the pipeline state is the same in every lane: keep it in scalars
+    auto uniform = [&]() __attribute__((always_inline)) {
+      pn = __builtin_amdgcn_readfirstlane(pn);
+      pns = __builtin_amdgcn_readfirstlane(pns);
+      pphase = __builtin_amdgcn_readfirstlane(pphase);
+      pSU = __builtin_amdgcn_readfirstlane(pSU);
+      pnU = __builtin_amdgcn_readfirstlane(pnU);
+      pnG = __builtin_amdgcn_readfirstlane(pnG);
+      pnu = __builtin_amdgcn_readfirstlane(pnu);
+      pb = __builtin_amdgcn_readfirstlane(pb);
+    };
     auto step_pre = [&]() __attribute__((always_inline)) {
+      uniform();
       if (!ctl && pn < pns) {
         if (pphase == 1) {
           wait_vm<0>();
@@ -365,6 +380,7 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p) {
       }
     };
     auto step_post = [&](int32_t grant) __attribute__((always_inline)) {
+      uniform();
       if (pn < pns) {
         if (pphase == 2) {
           if (!ctl) {
