@@ -469,6 +469,7 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p) {
         const int32_t hs = pd[0], nfar = pd[1], maxPt = pd[2], emax = pd[3], Pj = pd[4];
         const int64_t endj = (int64_t)(uint32_t)pd[5] | ((int64_t)pd[6] << 32);
         const bool need = maxPt >= cC && (int64_t)Pj + emax >= cC;
+        if (!need && cC > Pj) return true;           // no cell here and nothing to push
         const bool staged = need && (hs > 0 || nfar > 0);
         const int rb = (s & 1) * RB;
         const int64_t E = endj + 1;
