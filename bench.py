@@ -7,10 +7,14 @@ The graph itself is handed over (rc_graph_create) before the timed
 region, so the inputs are resident in HBM when timing starts.
 
 Prints one JSON line.  `value` is DP relaxations per second of wall time
-per step; `roofline` rates the DP fill kernel against the int32 VALU peak
-of MI355X with the fill time taken from HIP events that the library
-records on the fill's stream; `cpu_baseline` times the CPU oracle on the
-same graph on this host.
+per step; `roofline` rates the wavefront fill kernel against the packed
+16-bit VALU peak of MI355X (the table holds 16-bit cells and the kernel
+relaxes two cells per lane and instruction), with the kernel time taken
+from HIP events that the library records around that one launch on the
+fill's stream; `cpu_baseline` times the CPU oracle on the same graph on
+this host.  `--copy-calibration BYTES` instead runs one device-to-device
+copy of BYTES bytes (the reference kernel that scales rocprofv3's
+FETCH_SIZE / WRITE_SIZE counters to bytes) and exits.
 """
 
 import argparse
@@ -24,8 +28,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-# MI355X: 256 CUs, 64 int32 lanes per CU per clock, 2.4 GHz peak engine clock.
+# MI355X: 256 CUs, 4 SIMDs of 16 lanes each per CU (64 lane-ops per clock),
+# 2.4 GHz peak engine clock.  Packed 16-bit integer VALU instructions do two
+# operations per lane.
 VALU_INT32_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
+VALU_U16_PEAK_TOPS = 2 * VALU_INT32_PEAK_TOPS
 OPS_PER_RELAXATION = 3          # compare with tau, add dm, min into the target
 FILL_SOURCES = ["paper_1905_11722_amd/csrc/fill.hip", "paper_1905_11722_amd/csrc/blocked.hip",
                 "paper_1905_11722_amd/csrc/blocks.hip"]
@@ -42,14 +49,21 @@ def fill_source_hash():
 def read_traffic(workload):
     """HBM traffic of the fill from committed rocprofv3 PMC runs, if they were
     taken on the current fill source; else None."""
-    path = os.path.join(ROOT, "profiles", f"fill_{workload}_traffic.json")
+    path = os.path.join(ROOT, "profiles", f"k_fill_blocked_{workload}_traffic.txt")
     if not os.path.exists(path):
         return None
+    rec = {}
     with open(path) as f:
-        rec = json.load(f)
+        for line in f:
+            if "=" in line and not line.startswith((" ", "#", "`")):
+                k, v = line.split("=", 1)
+                rec[k.strip()] = v.strip()
     if rec.get("fill_source_sha256_16") != fill_source_hash():
         return None
-    return rec.get("bytes_per_solve")
+    try:
+        return int(rec["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def run_step(rcdp, g, case):
@@ -57,11 +71,12 @@ def run_step(rcdp, g, case):
     sol = fam.solve(case.B, case.objective)
     sched = sol.reconstruct() if sol.feasible else None
     fill_ms = sol.fill_ms()
+    kernel_ms = sol.fill_kernel_ms()
     info = fam.info
     t_star = sol.t_star
     sol.free()
     fam.free()
-    return info, fill_ms, t_star, sched
+    return info, fill_ms, kernel_ms, t_star, sched
 
 
 def time_case(rcdp, torch, case, steps, warmup):
@@ -69,11 +84,12 @@ def time_case(rcdp, torch, case, steps, warmup):
     for _ in range(warmup):
         run_step(rcdp, g, case)
     torch.cuda.synchronize()
-    fills = []
+    fills, kernels = [], []
     t0 = time.perf_counter()
     for _ in range(steps):
-        info, fill_ms, t_star, sched = run_step(rcdp, g, case)
+        info, fill_ms, kernel_ms, t_star, sched = run_step(rcdp, g, case)
         fills.append(fill_ms)
+        kernels.append(kernel_ms)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     g.free()
@@ -81,6 +97,10 @@ def time_case(rcdp, torch, case, steps, warmup):
         "ms_per_step": (t1 - t0) * 1e3 / steps,
         "fill_ms": sum(fills) / len(fills),
         "fill_ms_min": min(fills),
+        "kernel_ms": sum(kernels) / len(kernels),
+        "kernel_ms_min": min(kernels),
+        "kernel_ms_median": sorted(kernels)[len(kernels) // 2],
+        "kernel_ms_max": max(kernels),
         "info": info,
         "t_star": t_star,
         "k": None if sched is None else int(len(sched.chain)),
@@ -105,6 +125,20 @@ def cpu_baseline(case, relaxations):
     }
 
 
+def copy_calibration(nbytes):
+    """One device-to-device copy of nbytes: reads and writes nbytes of HBM."""
+    import torch
+    assert torch.cuda.is_available(), "the copy calibration needs a GPU"
+    n = nbytes // 4
+    src = torch.arange(n, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    assert bool((dst[-16:] == src[-16:]).all())
+    print(json.dumps({"copy_calibration_bytes": n * 4}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -113,7 +147,11 @@ def main():
     ap.add_argument("--workload", default="densenet121")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-other-graphs", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (--gpus {args.gpus} requested): the DP of one "
               "graph does not shard across GPUs; independent solves would.", file=sys.stderr)
@@ -133,7 +171,8 @@ def main():
     W = info["relaxations"]
     step_s = main_res["ms_per_step"] / 1e3
     fill_s = main_res["fill_ms"] / 1e3
-    achieved = OPS_PER_RELAXATION * W / fill_s / 1e12
+    kernel_s = main_res["kernel_ms"] / 1e3
+    achieved = OPS_PER_RELAXATION * W / kernel_s / 1e12
 
     per_graph = {}
     if not args.no_other_graphs:
@@ -163,7 +202,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "u32",
+        "dtype": "u16",
         "data": "synthetic",
         "config": {
             "workload": case.name,
@@ -182,15 +221,22 @@ def main():
         },
         "fill_ms": main_res["fill_ms"],
         "fill_relax_per_s": W / fill_s,
+        "fill_kernel_ms": {k: main_res[f"kernel_ms{s}"] for k, s in
+                           (("mean", ""), ("median", "_median"), ("min", "_min"),
+                            ("max", "_max"))},
         "roofline": {
             "bound": "alu",
             "achieved": achieved,
-            "peak": VALU_INT32_PEAK_TOPS,
-            "unit": "TOP/s (int32 VALU)",
-            "frac": achieved / VALU_INT32_PEAK_TOPS,
+            "peak": VALU_U16_PEAK_TOPS,
+            "unit": "TOP/s (packed 16-bit integer VALU)",
+            "frac": achieved / VALU_U16_PEAK_TOPS,
             "traffic": read_traffic(case.name),
-            "kernel": "DP fill of one solve (k_fill_blocked, or k_fill_level launches)",
+            "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE)",
+            "kernel": "k_fill_blocked (one launch per solve; the level path's launches "
+                      "when the family takes that path)",
+            "kernel_ms": main_res["kernel_ms"],
             "ops_per_relaxation": OPS_PER_RELAXATION,
+            "frac_of_int32_peak": achieved / VALU_INT32_PEAK_TOPS,
         },
         "per_graph": per_graph,
     }

@@ -150,6 +150,12 @@ int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solutio
 /* Milliseconds between HIP events recorded on the solve's stream just
  * before the first and just after the last DP-fill kernel of the solve. */
 int rc_solution_fill_ms(rc_solution s, float* ms);
+/* Milliseconds between HIP events recorded on the solve's stream just
+ * before and just after the one wavefront kernel of the blocked fill
+ * (without the kernels that prepare its records).  On the level path,
+ * which runs one launch per group of equal-size sets, this equals
+ * rc_solution_fill_ms.  Returns RC_OK or RC_E_ARG (NULL argument). */
+int rc_solution_fill_kernel_ms(rc_solution s, float* ms);
 
 /*
  * rc_reconstruct -- trace optarg back from (V, t*) (Section 4.2) and

@@ -642,9 +642,14 @@ __global__ void k_blocked_init(int32_t* progress, int32_t K, int32_t* ticket) {
 }
 
 template <int CPT>
-hipError_t launch_cpt(const BParams& prm, int32_t grid, hipStream_t s) {
+hipError_t launch_cpt(const BParams& prm, int32_t grid, hipEvent_t e0, hipEvent_t e1,
+                      hipStream_t s) {
+  if (e0 && hipEventRecord(e0, s) != hipSuccess) return hipErrorUnknown;
   hipLaunchKernelGGL(k_fill_blocked<CPT>, dim3(grid), dim3(kThreads), 0, s, prm);
-  return hipGetLastError();
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (e1 && hipEventRecord(e1, s) != hipSuccess) return hipErrorUnknown;
+  return hipSuccess;
 }
 
 int g_num_cus = -1;
@@ -718,9 +723,9 @@ hipError_t launch_fill_blocked(rc_solution sol, hipStream_t s) {
   if (std::getenv("RCDP_DEBUG"))
     std::fprintf(stderr, "rcdp: blocked fill K=%d columns of %d cells, grid=%d, %lld blocks\n", K,
                  C, grid, (long long)f->nblk);
-  if (cpt == 1) return launch_cpt<1>(prm, grid, s);
-  if (cpt == 2) return launch_cpt<2>(prm, grid, s);
-  return launch_cpt<4>(prm, grid, s);
+  if (cpt == 1) return launch_cpt<1>(prm, grid, sol->evk0, sol->evk1, s);
+  if (cpt == 2) return launch_cpt<2>(prm, grid, sol->evk0, sol->evk1, s);
+  return launch_cpt<4>(prm, grid, sol->evk0, sol->evk1, s);
 }
 
 }  // namespace rcdp

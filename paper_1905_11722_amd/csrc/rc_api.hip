@@ -428,6 +428,14 @@ void rc_family_free(rc_family f) {
 // Level launches suit narrow tables (few columns, many targets per level);
 // the persistent wavefront suits wide ones.  RCDP_FILL=level|wavefront
 // overrides the choice.
+static void destroy_events(rc_solution sol) {
+  for (hipEvent_t* e : {&sol->ev0, &sol->ev1, &sol->evk0, &sol->evk1})
+    if (*e) {
+      (void)hipEventDestroy(*e);
+      *e = nullptr;
+    }
+}
+
 static int choose_fill_path(rc_family f) {
   if (!f->has_records || f->F < 2) return 0;
   const char* env = std::getenv("RCDP_FILL");
@@ -456,8 +464,7 @@ int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solutio
   sol->arena.user = f->arena.user;
   auto fail = [&](int st) {
     (void)hipStreamSynchronize(s);
-    if (sol->ev0) (void)hipEventDestroy(sol->ev0);
-    if (sol->ev1) (void)hipEventDestroy(sol->ev1);
+    destroy_events(sol);
     sol->arena.release_all();
     delete sol;
     return st;
@@ -472,6 +479,9 @@ int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solutio
   if (hipEventCreate(&sol->ev0) != hipSuccess || hipEventCreate(&sol->ev1) != hipSuccess)
     return fail(RC_E_DEVICE);
   sol->fill_path = choose_fill_path(f);
+  if (sol->fill_path == 1 &&
+      (hipEventCreate(&sol->evk0) != hipSuccess || hipEventCreate(&sol->evk1) != hipSuccess))
+    return fail(RC_E_DEVICE);
   if (sol->fill_path == 1) {
     sol->progress = sol->arena.get_n<int32_t>(blocked_columns(f));
     sol->ticket = sol->arena.get_n<int32_t>(1);
@@ -511,6 +521,9 @@ int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solutio
     return fail(RC_E_DEVICE);
   }
   if (hipEventElapsedTime(&sol->fill_ms, sol->ev0, sol->ev1) != hipSuccess) sol->fill_ms = -1.f;
+  sol->kernel_ms = sol->fill_ms;
+  if (sol->evk0 && hipEventElapsedTime(&sol->kernel_ms, sol->evk0, sol->evk1) != hipSuccess)
+    sol->kernel_ms = -1.f;
   sol->t_star = hs.t_sel;
   sol->m_star = hs.t_sel >= 0 ? hs.m_sel : -1;
   sol->result = hs.t_sel >= 0 ? RC_OK : RC_INFEASIBLE;
@@ -523,6 +536,12 @@ int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solutio
 int rc_solution_fill_ms(rc_solution s, float* ms) {
   if (!s || !ms) return RC_E_ARG;
   *ms = s->fill_ms;
+  return RC_OK;
+}
+
+int rc_solution_fill_kernel_ms(rc_solution s, float* ms) {
+  if (!s || !ms) return RC_E_ARG;
+  *ms = s->kernel_ms;
   return RC_OK;
 }
 
@@ -596,8 +615,7 @@ int rc_export_table(rc_solution sol, int64_t first, int64_t count, int64_t* m_ho
 void rc_solution_free(rc_solution sol) {
   if (!sol) return;
   (void)hipDeviceSynchronize();
-  if (sol->ev0) (void)hipEventDestroy(sol->ev0);
-  if (sol->ev1) (void)hipEventDestroy(sol->ev1);
+  destroy_events(sol);
   sol->arena.release_all();
   delete sol;
 }

@@ -143,8 +143,10 @@ struct rc_solution_s {
   int32_t cpt = 1;                // blocked fill: cells per thread of a column
   uint16_t* sentinel = nullptr;   // 8 cells of infinity
   int32_t fill_path = 0;          // 0 level launches, 1 blocked wavefront
-  hipEvent_t ev0 = nullptr, ev1 = nullptr;
+  hipEvent_t ev0 = nullptr, ev1 = nullptr;    // around the whole fill
+  hipEvent_t evk0 = nullptr, evk1 = nullptr;  // around the wavefront kernel alone
   float fill_ms = 0.f;
+  float kernel_ms = 0.f;
 };
 
 namespace rcdp {

@@ -87,6 +87,8 @@ def load_library():
     lib.rc_solve.argtypes = [P, i64, i32, P, pp, ctypes.POINTER(i64), ctypes.POINTER(i64)]
     lib.rc_solution_fill_ms.restype = ctypes.c_int
     lib.rc_solution_fill_ms.argtypes = [P, ctypes.POINTER(ctypes.c_float)]
+    lib.rc_solution_fill_kernel_ms.restype = ctypes.c_int
+    lib.rc_solution_fill_kernel_ms.argtypes = [P, ctypes.POINTER(ctypes.c_float)]
     lib.rc_reconstruct.restype = ctypes.c_int
     lib.rc_reconstruct.argtypes = [P, P, ctypes.POINTER(i32), P, P, P, ctypes.POINTER(i64),
                                    ctypes.POINTER(i64), ctypes.POINTER(i64)]
@@ -269,6 +271,12 @@ class Solution:
     def fill_ms(self):
         ms = ctypes.c_float()
         _check(load_library().rc_solution_fill_ms(self._h, ctypes.byref(ms)), "rc_solution_fill_ms")
+        return ms.value
+
+    def fill_kernel_ms(self):
+        ms = ctypes.c_float()
+        _check(load_library().rc_solution_fill_kernel_ms(self._h, ctypes.byref(ms)),
+               "rc_solution_fill_kernel_ms")
         return ms.value
 
     def reconstruct(self):
