@@ -43,9 +43,10 @@
 //
 // Relaxation.  m' = x + dm if x <= tau (tau = B - c), else infinity, for two
 // targets at once in packed unsigned 16-bit lanes with saturation:
-// q = x -sat tau is nonzero exactly when the budget test fails, x +sat (-q)
-// then saturates to 0xFFFF, and adding dm keeps it there.  All finite
-// values stay below kPendM, so the saturated value is the infinity code.
+// y = x +sat dm, q = x -sat tau is nonzero exactly when the budget test
+// fails, and q * 0xFFFF +sat y (one multiply-add with clamp) is then 0xFFFF,
+// else y.  All finite values stay below kPendM, so the saturated value is
+// the infinity code.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -155,9 +156,11 @@ __device__ __forceinline__ u16x2 as_u16x2(int32_t v) { return __builtin_bit_cast
 
 // Two relaxations of Algorithm 1 (see the header comment).
 __device__ __forceinline__ u16x2 relax2(u16x2 acc, u16x2 x, u16x2 tau, u16x2 dm) {
+  const u16x2 y = __builtin_elementwise_add_sat(x, dm);
   const u16x2 q = __builtin_elementwise_sub_sat(x, tau);
-  const u16x2 y = __builtin_elementwise_add_sat(x, (u16x2)(0) - q);
-  return __builtin_elementwise_min(acc, __builtin_elementwise_add_sat(y, dm));
+  u16x2 r;
+  asm("v_pk_mad_u16 %0, %1, -1, %2 clamp" : "=v"(r) : "v"(q), "v"(y));
+  return __builtin_elementwise_min(acc, r);
 }
 
 // Does a chunk of 8 staged cells hold kUnset (not landed) / kPendM?
@@ -298,11 +301,11 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p) {
 #pragma unroll
         for (int kk = 0; kk < kNB; kk++) {
           const int4* h4 = reinterpret_cast<const int4*>(s_hdr[hb][kk]);
-          const int32_t emin = h4[0].y;
+          const int32_t a = s_hdr[hb][kk][7];
           const int4 tt = h4[4], dd = h4[5];
           const u16x2 tau[4] = {as_u16x2(tt.x), as_u16x2(tt.y), as_u16x2(tt.z), as_u16x2(tt.w)};
           const u16x2 dm[4] = {as_u16x2(dd.x), as_u16x2(dd.y), as_u16x2(dd.z), as_u16x2(dd.w)};
-          const uint16_t* wk = &s_win[wb][kk][(emin & 7) + tid];
+          const uint16_t* wk = &s_win[wb][kk][a + tid];
 #pragma unroll
           for (int q = 0; q < CPT; q++) {
             const u16x2 x = (u16x2)(wk[q * kBT]);
@@ -315,12 +318,11 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p) {
 #pragma unroll
       for (int kk = 0; kk < kNB; kk++) {
         const int4* h4 = reinterpret_cast<const int4*>(s_hdr[hb][kk]);
-        const int32_t emin = h4[0].y;
         const int4 o0 = h4[2], o1 = h4[3], tt = h4[4], dd = h4[5];
         const int32_t off[kJB] = {o0.x, o0.y, o0.z, o0.w, o1.x, o1.y, o1.z, o1.w};
         const u16x2 tau[4] = {as_u16x2(tt.x), as_u16x2(tt.y), as_u16x2(tt.z), as_u16x2(tt.w)};
         const u16x2 dm[4] = {as_u16x2(dd.x), as_u16x2(dd.y), as_u16x2(dd.z), as_u16x2(dd.w)};
-        const uint16_t* wk = &s_win[wb][kk][(emin & 7) + tid];
+        const uint16_t* wk = &s_win[wb][kk][tid];
 #pragma unroll
         for (int q = 0; q < CPT; q++)
 #pragma unroll
@@ -439,6 +441,7 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p) {
     };
     auto no_work = []() {};
     auto fail = [&]() {
+      wait_vm<0>();                                // no DMA may land after the exit
       if (ctl && lane == 0) p.st->error = 3;
     };
 
@@ -483,54 +486,9 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p) {
           }
         }
         long long t0 = 0;
-        // first step: the control stores the row and starts staging its reads
-        auto store_and_stage = [&]() __attribute__((always_inline)) {
-          const int64_t g = E - (int64_t)(c + 1) * C + (int64_t)CPL * lane;
-          if (g >= S) {                              // whole lines inside the row
-            const uint16_t* src = &s_push[rb + CPL * lane];
-            if constexpr (CPL == 4) {
-              st_sc1(p.m + g, *reinterpret_cast<const u32x2*>(src));
-            } else {
-#pragma unroll
-              for (int x = 0; x < CPL / 8; x++)
-                st_sc1(p.m + g + 8 * x, *reinterpret_cast<const u32x4*>(src + 8 * x));
-            }
-          }
-          if (!staged) return;
-          // halo: cells [u0 + C, u0 + C + hs) of row j; one window per far target
-          const u32x4 unset = (u32x4)(kUnset | (kUnset << 16));
-          const int nh = hs / 8;
-          if (lane < nh) *reinterpret_cast<u32x4*>(&s_push[rb + C + 8 * lane]) = unset;
-          for (int k = 0; k < nfar; k++)
-            for (int kc = lane; kc < NCF; kc += kWave)
-              *reinterpret_cast<u32x4*>(&s_push[2 * RB + k * FB + 8 * kc]) = unset;
-          wait_lds();
-          if (lane < nh) {
-            const int64_t gh = E - cC + 8 * lane;
-            const bool ok = gh >= S && gh + 8 <= E;
-            dma16(ok ? (const void*)(p.m + gh) : (const void*)p.sentinel,
-                  __builtin_amdgcn_readfirstlane(lds_addr(&s_push[rb + C])));
-          }
-          for (int k = 0; k < nfar; k++) {
-            const int32_t e = pd[8 + k];
-            const int64_t astart = endj + u0 + e - (e & 7);
-#pragma unroll
-            for (int i = 0; i < (NCF + 63) / 64; i++) {
-              const int kc = lane + 64 * i;
-              if (kc < NCF) {
-                const int64_t gf = astart + 8 * (int64_t)kc;
-                const bool ok = gf >= S && gf + 8 <= E;
-                dma16(ok ? (const void*)(p.m + gf) : (const void*)p.sentinel,
-                      __builtin_amdgcn_readfirstlane(lds_addr(&s_push[2 * RB + k * FB + 512 * i])));
-              }
-            }
-          }
-          t0 = wall_clock64();
-        };
-        // later steps: inspect the staged chunks, reload those that read a
-        // cell not written yet, report the row ready when all have landed
-        auto inspect = [&]() __attribute__((always_inline)) {
-          if (rr >= s) return;
+        // reload the staged chunks that read a cell not written yet; report
+        // the row ready when all have landed
+        auto inspect_now = [&]() __attribute__((always_inline)) {
           bool unset = false;
           const int nh = hs / 8;
           if (lane < nh) {
@@ -570,6 +528,58 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p) {
             cur_set(0, s);
           else if (wall_clock64() - t0 > p.timeout_ticks)
             cur_set(1, 1);
+        };
+        // first step: the control stores the row and starts staging its reads
+        auto store_and_stage = [&]() __attribute__((always_inline)) {
+          const int64_t g = E - (int64_t)(c + 1) * C + (int64_t)CPL * lane;
+          if (g >= S) {                              // whole lines inside the row
+            const uint16_t* src = &s_push[rb + CPL * lane];
+            if constexpr (CPL == 4) {
+              st_sc1(p.m + g, *reinterpret_cast<const u32x2*>(src));
+            } else {
+#pragma unroll
+              for (int x = 0; x < CPL / 8; x++)
+                st_sc1(p.m + g + 8 * x, *reinterpret_cast<const u32x4*>(src + 8 * x));
+            }
+          }
+          if (staged) {
+            // halo: cells [u0 + C, u0 + C + hs) of row j, after the row's own
+            // cells; one window per far target
+            const u32x4 unset = (u32x4)(kUnset | (kUnset << 16));
+            const int nh = hs / 8;
+            if (lane < nh) *reinterpret_cast<u32x4*>(&s_push[rb + C + 8 * lane]) = unset;
+            for (int k = 0; k < nfar; k++)
+              for (int kc = lane; kc < NCF; kc += kWave)
+                *reinterpret_cast<u32x4*>(&s_push[2 * RB + k * FB + 8 * kc]) = unset;
+            wait_lds();
+            if (lane < nh) {
+              const int64_t gh = E - cC + 8 * lane;
+              const bool ok = gh >= S && gh + 8 <= E;
+              dma16(ok ? (const void*)(p.m + gh) : (const void*)p.sentinel,
+                    __builtin_amdgcn_readfirstlane(lds_addr(&s_push[rb + C])));
+            }
+            for (int k = 0; k < nfar; k++) {
+              const int32_t e = pd[8 + k];
+              const int64_t astart = endj + u0 + e - (e & 7);
+#pragma unroll
+              for (int i = 0; i < (NCF + 63) / 64; i++) {
+                const int kc = lane + 64 * i;
+                if (kc < NCF) {
+                  const int64_t gf = astart + 8 * (int64_t)kc;
+                  const bool ok = gf >= S && gf + 8 <= E;
+                  dma16(ok ? (const void*)(p.m + gf) : (const void*)p.sentinel,
+                        __builtin_amdgcn_readfirstlane(
+                            lds_addr(&s_push[2 * RB + k * FB + 512 * i])));
+                }
+              }
+            }
+          }
+          if (staged) t0 = wall_clock64();
+        };
+        // later steps: inspect the staged chunks until the row is ready
+        auto inspect = [&]() __attribute__((always_inline)) {
+          if (rr >= s) return;
+          inspect_now();
         };
         if (!run_step(store_and_stage)) return false;
         if (staged)

@@ -188,7 +188,9 @@ __global__ __launch_bounds__(256) void k_blk_clusters(const int64_t* rec_ptr, Bl
 // per shift cluster that has such a slot, compacted from clu_ptr[b] on.  A
 // compact record is kRecInts int32: [0] source i, [1] smallest shift emin,
 // [2] staged span emax - emin (<= kSpan), [3] P_i = w_i - 1, [4..5] index of
-// the cell u = 0 of row i (int64), [6] emax, [8 + s] shift - emin of slot s,
+// the cell u = 0 of row i (int64), [6] emax, [7] a = emin mod 8 (the
+// window starts on a 16-byte boundary, a cells before the cell of shift
+// emin), [8 + s] a + shift - emin of slot s (its cell in the window),
 // [16 + p] budgets B - c of slots 2p, 2p+1 as two uint16, [20 + p] the
 // additions dm of slots 2p, 2p+1 as two uint16.  A slot without a live pair
 // gets budget 0 and addition 0xFFFF, so its candidate always saturates to
@@ -249,7 +251,7 @@ __global__ __launch_bounds__(256) void k_rec_prepare(int64_t F, int32_t Beff, co
       for (int s = 0; s < kJB; s++) {
         const int32_t tau = Beff - R.c[(base + r) * kJB + s];
         const bool ok = cl[s] == k && tau >= 0;
-        d[8 + s] = ok ? e[s] - emin : 0;
+        d[8 + s] = (emin & 7) + (ok ? e[s] - emin : 0);
         const uint32_t tv = ok ? (uint32_t)tau : 0u;
         const uint32_t dv = ok ? (R.kadd[(base + r) * kJB + s] >> 16) : 0xFFFFu;
         tau2[s / 2] |= tv << (16 * (s & 1));
@@ -262,7 +264,7 @@ __global__ __launch_bounds__(256) void k_rec_prepare(int64_t F, int32_t Beff, co
       d[4] = (int32_t)(endi & 0xFFFFFFFF);
       d[5] = (int32_t)(endi >> 32);
       d[6] = emax;
-      d[7] = 0;
+      d[7] = emin & 7;
       for (int x = 0; x < kJB / 2; x++) {
         d[16 + x] = (int32_t)tau2[x];
         d[20 + x] = (int32_t)dm2[x];

@@ -225,6 +225,25 @@ def test_wavefront_column_widths(rc, oracle_mod, monkeypatch, cpt, n, p, seed):
             compare(rc, oracle_mod, g, mode, B)
 
 
+@pytest.mark.parametrize("seed", [10, 12, 16])
+def test_wavefront_repeated_solves(rc, oracle_mod, monkeypatch, seed):
+    """The same wide tables solved repeatedly: the persistent fill's columns
+    meet in a different interleaving each time, and every table must match."""
+    monkeypatch.setenv("RCDP_FILL", "wavefront")
+    g = W.random_dag(12, 0.2, 5000 + seed, tmax=700, mmax=60)
+    lo, hi = 2 * max(g.M), 2 * sum(g.M)
+    for B in (lo, (2 * lo + hi) // 3, hi):
+        for mode in ("exact", "pruned"):
+            ref = oracle_mod.solve(g, mode, B, "tc")
+            rm, _ = ref.table()
+            fam = rc.Graph.create(g).build_family(mode)
+            for rep in range(4):
+                sol = fam.solve(B, "tc")
+                m, _ = sol.table()
+                np.testing.assert_array_equal(m, rm, err_msg=f"B={B} {mode} repetition {rep}")
+                sol.free()
+
+
 @pytest.mark.parametrize("path", ["level", "wavefront"])
 def test_fill_paths_long_chain(rc, oracle_mod, monkeypatch, path):
     """A long chain: one target per level, rows of many columns."""
