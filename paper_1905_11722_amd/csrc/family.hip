@@ -104,6 +104,51 @@ __global__ __launch_bounds__(1024) void k_ancestors(int n, int words, int num_de
   }
 }
 
+// Small graphs: one wave walks the nodes in depth order (a topological
+// order) with the masks, the depth order and the predecessor lists in LDS;
+// lane w owns word w of every mask.  A node's predecessors are all earlier
+// in the order, and one wave's LDS accesses complete in order, so the walk
+// needs no barrier at all (the depth-parallel sweep pays one per depth).
+__global__ __launch_bounds__(64) void k_ancestors_wave(int n, int words, int num_edges,
+                                                       const int32_t* by_depth,
+                                                       const int32_t* pred_ptr,
+                                                       const int32_t* pred_idx,
+                                                       uint64_t* anc_out) {
+  extern __shared__ uint64_t lds_anc[];
+  uint64_t* anc = lds_anc;
+  int32_t* l_pp = reinterpret_cast<int32_t*>(lds_anc + (int64_t)n * words);
+  int32_t* l_pi = l_pp + (n + 1);
+  int32_t* l_bd = l_pi + num_edges;
+  const int lane = threadIdx.x;
+  for (int x = lane; x <= n; x += kWave) l_pp[x] = pred_ptr[x];
+  for (int x = lane; x < num_edges; x += kWave) l_pi[x] = pred_idx[x];
+  for (int x = lane; x < n; x += kWave) l_bd[x] = by_depth[x];
+  __syncthreads();
+  const bool active = lane < words;
+  if (n == 0) return;
+  int v = l_bd[0];
+  int q0 = l_pp[v], q1 = l_pp[v + 1];
+  for (int idx = 0; idx < n; idx++) {
+    const int vn = idx + 1 < n ? l_bd[idx + 1] : v;     // the next node, ahead
+    uint64_t x = (v >> 6) == lane ? (1ull << (v & 63)) : 0ull;
+    int q = q0;
+    for (; q + 4 <= q1; q += 4) {
+      const int a0 = l_pi[q], a1 = l_pi[q + 1], a2 = l_pi[q + 2], a3 = l_pi[q + 3];
+      if (active)
+        x |= anc[(int64_t)a0 * words + lane] | anc[(int64_t)a1 * words + lane] |
+             anc[(int64_t)a2 * words + lane] | anc[(int64_t)a3 * words + lane];
+    }
+    for (; q < q1; q++)
+      if (active) x |= anc[(int64_t)l_pi[q] * words + lane];
+    if (active) anc[(int64_t)v * words + lane] = x;
+    q0 = l_pp[vn];
+    q1 = l_pp[vn + 1];
+    v = vn;
+  }
+  __syncthreads();
+  for (int it = lane; it < n * words; it += kWave) anc_out[it] = anc[it];
+}
+
 // Candidates of the pruned family, set-major: [0] = empty set,
 // [1 + v] = L^v, [n + 1] = V.
 __global__ void k_pruned_candidates(int n, int words, const uint64_t* anc, uint64_t* cand) {
@@ -279,10 +324,25 @@ __global__ __launch_bounds__(1024) void k_rank_pruned(int words, int n, const ui
 //   and (iv) of Eq. 2 for the set L' = L (for a lower set L the
 //   predecessors of delta+(L) inside L add nothing outside L)
 //   w_L = T(L \ boundary(L)) + 1, the cells of row L that can be finite.
+template <bool kLds>
 __global__ __launch_bounds__(256) void k_set_quantities(
-    int64_t F, int words, int64_t fstride, const uint64_t* bits, const uint64_t* succ,
-    const uint64_t* pred, const int32_t* T, const int32_t* M, uint64_t* bd, int32_t* size,
+    int64_t F, int n, int words, int64_t fstride, const uint64_t* bits, const uint64_t* succ_g,
+    const uint64_t* pred_g, const int32_t* T, const int32_t* M, uint64_t* bd, int32_t* size,
     int32_t* Tsum, int32_t* Msum, int32_t* Tbd, int32_t* Mbd, int32_t* A, int32_t* w_out) {
+  // small graphs: the successor and predecessor masks of every node in LDS
+  extern __shared__ uint64_t lds_nb[];
+  const uint64_t* succ = succ_g;
+  const uint64_t* pred = pred_g;
+  if (kLds) {
+    const int64_t cnt = (int64_t)n * words;
+    for (int64_t x = threadIdx.x; x < cnt; x += blockDim.x) {
+      lds_nb[x] = succ_g[x];
+      lds_nb[cnt + x] = pred_g[x];
+    }
+    __syncthreads();
+    succ = lds_nb;
+    pred = lds_nb + cnt;
+  }
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t s = blockIdx.x * (int64_t)(blockDim.x / kWave) + threadIdx.x / kWave;
   if (s >= F) return;
@@ -496,6 +556,13 @@ hipError_t launch_graph_masks(rc_graph g, const int32_t* d_row_ptr, const int32_
 }
 
 hipError_t launch_ancestors(rc_graph g, uint64_t* anc, hipStream_t s) {
+  const size_t lds_wave = sizeof(uint64_t) * (size_t)g->n * g->words +
+                          sizeof(int32_t) * ((size_t)g->n + 1 + g->num_pred_edges + g->n);
+  if (lds_wave <= 64 * 1024) {
+    hipLaunchKernelGGL(k_ancestors_wave, dim3(1), dim3(kWave), lds_wave, s, g->n, g->words,
+                       g->num_pred_edges, g->dByDepth, g->dPredPtr, g->dPredIdx, anc);
+    return hipGetLastError();
+  }
   const size_t lds = sizeof(uint64_t) * (size_t)g->n * g->words +
                      sizeof(int32_t) * ((size_t)g->n + 1 + g->num_pred_edges + g->n +
                                         g->num_depths + 1);
@@ -544,9 +611,16 @@ hipError_t launch_rank(rc_graph g, int32_t mode, const uint64_t* cand, int64_t n
 hipError_t launch_set_quantities(rc_family f, hipStream_t s) {
   rc_graph g = f->g;
   const int per_block = 256 / kWave;
-  hipLaunchKernelGGL(k_set_quantities, dim3((unsigned)((f->F + per_block - 1) / per_block)),
-                     dim3(256), 0, s, f->F, g->words, f->fstride, f->bits, g->dSucc, g->dPred,
-                     g->dT, g->dM, f->bd, f->size, f->Tsum, f->Msum, f->Tbd, f->Mbd, f->A, f->w);
+  const dim3 grid((unsigned)((f->F + per_block - 1) / per_block));
+  const size_t lds = 2 * sizeof(uint64_t) * (size_t)g->n * g->words;
+  if (lds <= 64 * 1024)
+    hipLaunchKernelGGL(k_set_quantities<true>, grid, dim3(256), lds, s, f->F, g->n, g->words,
+                       f->fstride, f->bits, g->dSucc, g->dPred, g->dT, g->dM, f->bd, f->size,
+                       f->Tsum, f->Msum, f->Tbd, f->Mbd, f->A, f->w);
+  else
+    hipLaunchKernelGGL(k_set_quantities<false>, grid, dim3(256), 0, s, f->F, g->n, g->words,
+                       f->fstride, f->bits, g->dSucc, g->dPred, g->dT, g->dM, f->bd, f->size,
+                       f->Tsum, f->Msum, f->Tbd, f->Mbd, f->A, f->w);
   return hipGetLastError();
 }
 

@@ -162,7 +162,7 @@ __global__ void k_select_finish(const uint16_t* m, const int64_t* row_off, int64
 // (ascending family index, kTraceThreads at a time) for optarg[L', t']:
 // the smallest index whose cell passes the budget test and reproduces the
 // target value.  The re-evaluation runs on wave 0, lane w holding word w.
-constexpr int kTraceThreads = 256;
+constexpr int kTraceThreads = 512;
 constexpr int kTraceLds = 2048;       // families up to this size keep their per-set arrays in LDS
 
 __global__ __launch_bounds__(kTraceThreads) void k_trace(
@@ -195,6 +195,16 @@ __global__ __launch_bounds__(kTraceThreads) void k_trace(
       s_pp[x] = pred_ptr[x];
     }
     if (tid == 0) s_pp[F] = pred_ptr[F];
+  }
+  // Every step of the walk reads the predecessor lists of one set: bring
+  // them all into this CU's L2 first when they are small (a few MB), so that
+  // those reads cost an L2 hit instead of a trip to memory.
+  const int64_t P = pred_ptr[F];
+  if (P <= ((int64_t)1 << 17)) {
+    int32_t acc = 0;
+    for (int64_t x = tid * 16; x < P; x += kTraceThreads * 16)
+      acc ^= pidx[x] ^ pdt[x] ^ pc[x] ^ pdm[x];
+    if (acc == 0x7fffffff) st->pad0 = acc;          // keeps the loads
   }
   __syncthreads();
   auto Wd = [&](int64_t i) { return in_lds ? s_w[i] : w[i]; };
@@ -272,7 +282,7 @@ __global__ __launch_bounds__(kTraceThreads) void k_trace(
   if (tid >= kWave) return;
   // Eq. 2 per segment: M(U_{i-1}) + 2 M(V_i) + A(L_i), U grows by the
   // boundary of each L_i; the loads of kPre chain steps are issued together
-  constexpr int kPre = 4;
+  constexpr int kPre = 16;
   const bool active = lane < words;
   uint64_t U = 0, prev = 0;
   int64_t mu = 0, peak = 0;
