@@ -130,6 +130,20 @@ int rc_family_stats(rc_family f, rc_family_info* info);
 /* Family members as bitmasks: bits_host[s * words + w] holds nodes
  * 64w..64w+63 of set s (bit v % 64), s in family order. */
 int rc_family_sets(rc_family f, uint64_t* bits_host, void* stream);
+/*
+ * rc_min_budget -- the smallest budget B for which the family admits a
+ * strategy (Section 5 runs its experiments at this budget and finds it by
+ * binary search).  Computed on the device: B is feasible exactly when the
+ * t-free form of Algorithm 1 (f[empty] = 0, f[L'] = min of f[L] + dm over the
+ * pairs L < L' with f[L] + c(L, L') <= B; the row minima of the opt table)
+ * reaches V, feasibility is monotone in B, and B = 2 M(V) is always feasible,
+ * so the search runs over [0, 2 M(V)] with 64 budgets per round.
+ *  *B_min: that budget (rc_solve(f, *B_min, ...) is feasible, *B_min - 1 is
+ *  not).  Synchronises stream.
+ * Returns RC_OK, RC_E_ARG (NULL argument), RC_E_OVERFLOW (2 M(V) >= 2^31 - 1),
+ * RC_E_NOMEM, RC_E_DEVICE.
+ */
+int rc_min_budget(rc_family f, void* stream, int64_t* B_min);
 void rc_family_free(rc_family f);
 
 /*

@@ -167,3 +167,22 @@ def solve(graph, mode, B, objective="tc", max_sets=1 << 20, max_sources=-1, csr=
     if not h:
         raise MemoryError("oracle_solve returned NULL")
     return OracleResult(graph, h)
+
+
+def min_budget(graph, mode):
+    """The smallest budget B for which the family admits a strategy.
+
+    Section 5 runs its experiments at this budget and finds it by binary
+    search.  Feasibility is monotone in B (a strategy whose peak is within B
+    is within every larger budget) and B = 2 M(V) is always feasible (the
+    one-segment chain {V} peaks at 2 M(V), Eq. 2), so bisection over
+    [0, 2 M(V)] on whether Algorithm 1 finds a finite cell in row V gives it.
+    """
+    lo, hi = -1, 2 * int(sum(graph.M))
+    while hi - lo > 1:
+        mid = (lo + hi) // 2
+        if solve(graph, mode, mid, "tc").status == OK:
+            hi = mid
+        else:
+            lo = mid
+    return hi

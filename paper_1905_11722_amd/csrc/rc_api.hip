@@ -403,6 +403,24 @@ int rc_family_stats(rc_family f, rc_family_info* info) {
   return RC_OK;
 }
 
+int rc_min_budget(rc_family f, void* stream, int64_t* B_min) {
+  if (!f || !B_min) return RC_E_ARG;
+  const int64_t hi0 = 2 * f->g->M_total;           // the chain {V} peaks at 2 M(V)
+  if (hi0 >= INT32_MAX) return RC_E_OVERFLOW;
+  hipStream_t s = as_stream(stream);
+  const size_t scratch = min_budget_scratch_bytes(f, (int32_t)hi0);
+  if (scratch > 0 && !f->bmin_scratch) {
+    f->bmin_scratch = static_cast<uint32_t*>(f->arena.get(scratch));
+    if (!f->bmin_scratch) return RC_E_NOMEM;
+  }
+  RC_HIP(launch_min_budget(f, (int32_t)hi0, f->bmin_scratch, s));
+  DevStatus hs;
+  RC_HIP(hipMemcpyAsync(&hs, f->status, sizeof(hs), hipMemcpyDeviceToHost, s));
+  RC_HIP(hipStreamSynchronize(s));
+  *B_min = hs.bmin;
+  return RC_OK;
+}
+
 int rc_family_sets(rc_family f, uint64_t* bits_host, void* stream) {
   if (!f || !bits_host) return RC_E_ARG;
   const int words = f->g->words;

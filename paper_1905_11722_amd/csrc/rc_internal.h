@@ -55,6 +55,7 @@ struct DevStatus {
   int32_t k;             // chain length
   int32_t pad0;
   int64_t overhead, peak, cache_mem;
+  int64_t bmin;          // smallest feasible budget (rc_min_budget)
 };
 
 // Panel / triangle records of the blocked fill (blocks.hip).
@@ -112,6 +113,7 @@ struct rc_family_s {
   int64_t clu_total = 0;
   rcdp::BlockRecords rec;
   rcdp::DevStatus* status = nullptr;
+  uint32_t* bmin_scratch = nullptr; // rc_min_budget: f values of large families
   // host copies used for launches
   std::vector<int64_t> level_ptr; // family index ranges of equal set size
   std::vector<int32_t> level_maxw;
@@ -197,6 +199,10 @@ hipError_t launch_rec_sort(rc_solution sol, int32_t C, hipStream_t s);
 hipError_t launch_fill_pending(rc_solution sol, hipStream_t s);
 hipError_t launch_pad_init(rc_solution sol, hipStream_t s);
 int blocked_cells_per_thread(rc_family f);
+
+// ---- smallest feasible budget (budget.hip)
+size_t min_budget_scratch_bytes(rc_family f, int32_t hi0);
+hipError_t launch_min_budget(rc_family f, int32_t hi0, uint32_t* scratch, hipStream_t s);
 int64_t blocked_columns(rc_family f);
 hipError_t launch_fill_blocked(rc_solution sol, hipStream_t s);
 

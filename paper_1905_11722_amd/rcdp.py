@@ -87,6 +87,8 @@ def load_library():
     lib.rc_solve.argtypes = [P, i64, i32, P, pp, ctypes.POINTER(i64), ctypes.POINTER(i64)]
     lib.rc_solution_fill_ms.restype = ctypes.c_int
     lib.rc_solution_fill_ms.argtypes = [P, ctypes.POINTER(ctypes.c_float)]
+    lib.rc_min_budget.restype = ctypes.c_int
+    lib.rc_min_budget.argtypes = [P, ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64)]
     lib.rc_solution_fill_kernel_ms.restype = ctypes.c_int
     lib.rc_solution_fill_kernel_ms.argtypes = [P, ctypes.POINTER(ctypes.c_float)]
     lib.rc_reconstruct.restype = ctypes.c_int
@@ -231,6 +233,17 @@ class Family:
         for v in range(n):
             out[:, v] = (buf[:, v // 64] >> np.uint64(v % 64)) & np.uint64(1)
         return out
+
+    def min_budget(self):
+        """The smallest budget with a strategy in this family (rc_min_budget)."""
+        b = ctypes.c_int64(-1)
+        _check(load_library().rc_min_budget(self._h, _stream(), ctypes.byref(b)), "rc_min_budget")
+        return b.value
+
+    def sweep(self, budgets, objective="mc"):
+        """Solve at each budget in turn: [(budget, Solution)].  The memory-centric
+        sweep of Section 4.4 runs the same family at a range of budgets."""
+        return [(int(B), self.solve(int(B), objective)) for B in budgets]
 
     def solve(self, B, objective="tc"):
         lib = load_library()

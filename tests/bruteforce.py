@@ -174,3 +174,31 @@ def select(opt, F, objective):
     if not ts:
         return None
     return min(ts) if objective == "tc" else max(ts)
+
+
+def brute_min_budget(g, mode, max_chains=5_000_000):
+    """The smallest budget with a strategy: the least Eq. 2 peak over every
+    chain of family sets from the empty set to V, by enumeration."""
+    sg = SetGraph(g)
+    F = family(sg, mode)
+    supers = [[j for j, S2 in enumerate(F) if S2 != S and S & ~S2 == 0] for S in F]
+    bd = [sg.boundary(S) for S in F]
+    v = len(F) - 1
+    best = None
+    count = 0
+    stack = [(0, 0, 0)]           # (family index of last set, U so far, peak so far)
+    while stack:
+        i, U, peak = stack.pop()
+        if i == v:
+            best = peak if best is None else min(best, peak)
+            continue
+        L = F[i]
+        for j in supers[i]:
+            p2 = max(peak, sg.segment_memory(U, L, F[j]))
+            if best is not None and p2 >= best:
+                continue
+            count += 1
+            if count > max_chains:
+                raise RuntimeError("too many chains for brute force")
+            stack.append((j, U | bd[j], p2))
+    return 0 if v == 0 else best

@@ -251,3 +251,67 @@ def test_fill_paths_long_chain(rc, oracle_mod, monkeypatch, path):
     g = W.chain(60, seed=9, tmax=400, mmax=30)
     for B in (2 * max(g.M), sum(g.M) // 3, sum(g.M), 2 * sum(g.M)):
         compare(rc, oracle_mod, g, "exact", B)
+
+
+@pytest.mark.parametrize("n,p,seed", RANDOM[:16])
+@pytest.mark.parametrize("mode", ["exact", "pruned"])
+def test_min_budget_random(rc, oracle_mod, n, p, seed, mode):
+    """rc_min_budget against the oracle's bisection (Section 5)."""
+    g = W.random_dag(n, p, 1000 + seed, tmax=40, mmax=30)
+    fam = rc.Graph.create(g).build_family(mode)
+    assert fam.min_budget() == oracle_mod.min_budget(g, mode)
+
+
+@pytest.mark.parametrize("name", ["chain16", "layered24", "ladder40", "unet", "resnet50",
+                                  "densenet121"])
+def test_min_budget_workloads(rc, name):
+    """At every workload: the budget found is feasible and one less is not,
+    both decided by the GPU solve; no budget below 2 max M_v can be feasible."""
+    c = W.case(name)
+    fam = rc.Graph.create(c.graph).build_family(c.mode)
+    b = fam.min_budget()
+    assert 2 * max(c.graph.M) <= b <= 2 * sum(c.graph.M)
+    assert fam.solve(b, "tc").feasible
+    assert not fam.solve(b - 1, "tc").feasible
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", ["layered24", "unet", "resnet50"])
+def test_min_budget_oracle_full(rc, oracle_mod, name):
+    c = W.case(name)
+    fam = rc.Graph.create(c.graph).build_family(c.mode)
+    assert fam.min_budget() == oracle_mod.min_budget(c.graph, c.mode)
+
+
+def mc_budgets(b_min, m_total, count=32):
+    """Budgets of the memory-centric sweep: count points from the smallest
+    feasible budget to 2 M(V), where the one-segment chain is feasible."""
+    top = 2 * m_total
+    return [b_min + (j * (top - b_min)) // (count - 1) for j in range(count)]
+
+
+def test_mc_sweep_resnet50(rc, oracle_mod):
+    """The memory-centric sweep of the ResNet-50-shaped graph over 32 budgets
+    (Section 4.4): t_MC never decreases with the budget, every traced schedule
+    re-evaluates to its own t and stays within its budget, the sweep ends at
+    t_MC = T(V) at B = 2 M(V), and sampled budgets match the oracle."""
+    c = W.case("resnet50")
+    g = c.graph
+    fam = rc.Graph.create(g).build_family("pruned")
+    b_min = fam.min_budget()
+    budgets = mc_budgets(b_min, sum(g.M))
+    prev = -1
+    for j, (B, sol) in enumerate(fam.sweep(budgets, "mc")):
+        assert sol.feasible
+        sched = sol.reconstruct()
+        assert sched.overhead == sol.t_star
+        assert sched.peak <= B
+        assert sol.t_star >= prev
+        prev = sol.t_star
+        if j in (0, 11, 31):
+            ref = oracle_mod.solve(g, "pruned", B, "mc")
+            assert (sol.t_star, sol.m_star) == (ref.t_star, ref.m_star)
+            chain, _, _ = ref.schedule()
+            np.testing.assert_array_equal(sched.chain, chain)
+        sol.free()
+    assert prev == sum(g.T)

@@ -110,3 +110,16 @@ def test_empty_graph(oracle_mod):
     assert (r.num_sets, r.T_total, r.t_star, r.m_star, r.k) == (1, 0, 0, 0, 0)
     r = oracle_mod.solve(g, "pruned", 0)
     assert (r.num_sets, r.t_star, r.k) == (1, 0, 0)
+
+
+@pytest.mark.parametrize("n,p,seed", CASES[:12])
+@pytest.mark.parametrize("mode", ["exact", "pruned"])
+def test_min_budget(oracle_mod, n, p, seed, mode):
+    """The oracle's bisection for the smallest feasible budget (Section 5)
+    against the least peak over every chain."""
+    g = W.random_dag(n, p, seed, tmax=9, mmax=7)
+    b = oracle_mod.min_budget(g, mode)
+    assert b == bf.brute_min_budget(g, mode)
+    assert b >= 2 * max(g.M)                       # every node lies in a segment
+    assert oracle_mod.solve(g, mode, b, "tc").status == oracle_mod.OK
+    assert oracle_mod.solve(g, mode, b - 1, "tc").status == oracle_mod.INFEASIBLE

@@ -74,6 +74,7 @@ def test_chain16_at_64(oracle_mod):
     assert oracle_mod.solve(g, "exact", c.B, "mc").t_star == max(best) == 92
     bmin = min(peak for _, peak, _ in chain_strategies(g.T, g.M))
     assert bmin == 45
+    assert oracle_mod.min_budget(g, "exact") == bmin
     assert oracle_mod.solve(g, "exact", bmin, "tc").status == oracle_mod.OK
     assert oracle_mod.solve(g, "exact", bmin - 1, "tc").status == oracle_mod.INFEASIBLE
 
