@@ -33,7 +33,7 @@ MIB = 1 << 20
 
 __all__ = [
     "Graph", "Case", "chain", "layered", "ladder", "resnet50", "densenet121",
-    "unet", "random_dag", "antichain", "CASES", "case", "PAPER_COST_CONVENTION",
+    "unet", "random_dag", "antichain", "CASES", "case", "PAPER_COST_CONVENTION", "paper_costs",
 ]
 
 
@@ -417,6 +417,14 @@ def unet(batch=8, image=572, base=64, depth=4):
 PAPER_COST_CONVENTION = "T_v = 10 for conv, 1 otherwise (Section 3)"
 
 
+def paper_costs(g):
+    """The same graph with the forward times of the paper's experiments: T_v
+    = 10 for convolution nodes (transposed ones included) and 1 for every
+    other node (end of Section 3); memory sizes unchanged."""
+    T = [10 if op in ("conv", "upconv") else 1 for op in g.ops]
+    return Graph(g.n, [list(x) for x in g.succ], T, list(g.M), list(g.names), list(g.ops))
+
+
 def _cases():
     return {
         "chain16": lambda: Case("chain16", chain(16, 0), "exact", 64, "tc",
@@ -431,6 +439,14 @@ def _cases():
                              "U-Net shape, batch 8, 572^2, pruned family, B=16384"),
         "ladder40": lambda: Case("ladder40", ladder(20, 0), "exact", 1024, "tc",
                                  "2x20 ladder, cross edge every 2 nodes, exact family, B=1024"),
+        "resnet50_t10": lambda: Case("resnet50_t10", paper_costs(resnet50(32, 224)), "pruned",
+                                     4096, "tc", "ResNet-50 shape with T_v = 10 (conv) / 1, "
+                                     "pruned family, B=4096"),
+        "densenet121_t10": lambda: Case("densenet121_t10", paper_costs(densenet121(32, 224)),
+                                        "pruned", 4096, "tc", "DenseNet-121 shape with T_v = 10 "
+                                        "(conv) / 1, pruned family, B=4096"),
+        "unet_t10": lambda: Case("unet_t10", paper_costs(unet(8, 572)), "pruned", 16384, "tc",
+                                 "U-Net shape with T_v = 10 (conv) / 1, pruned family, B=16384"),
     }
 
 

@@ -315,3 +315,15 @@ def test_mc_sweep_resnet50(rc, oracle_mod):
             np.testing.assert_array_equal(sched.chain, chain)
         sol.free()
     assert prev == sum(g.T)
+
+
+@pytest.mark.parametrize("name", ["resnet50_t10", "densenet121_t10", "unet_t10"])
+def test_paper_cost_convention(rc, oracle_mod, name):
+    """The CNN-shaped graphs with the forward times of the paper's experiments
+    (T_v = 10 for convolutions, 1 otherwise): narrow tables, whole table and
+    both objectives against the oracle, at the case budget and at the
+    smallest feasible one."""
+    c = W.case(name)
+    compare(rc, oracle_mod, c.graph, c.mode, c.B)
+    fam = rc.Graph.create(c.graph).build_family(c.mode)
+    compare(rc, oracle_mod, c.graph, c.mode, fam.min_budget())
