@@ -35,9 +35,7 @@ void set_last_error_msg(const char* msg) {
   std::snprintf(g_last_error, sizeof(g_last_error), "%s", msg);
 }
 
-void* Arena::get(size_t bytes) {
-  if (bytes == 0) bytes = 1;
-  bytes = (bytes + 255) & ~size_t(255);
+void* Arena::raw(size_t bytes) {
   void* p = nullptr;
   if (alloc) {
     p = alloc(bytes, user);
@@ -48,7 +46,25 @@ void* Arena::get(size_t bytes) {
   return p;
 }
 
+// Small buffers are carved from chunks of kChunk bytes, so that a handle
+// costs a few calls of the caller's allocator rather than one per buffer.
+void* Arena::get(size_t bytes) {
+  if (bytes == 0) bytes = 1;
+  bytes = (bytes + 255) & ~size_t(255);
+  if (bytes > kChunk / 4) return raw(bytes);
+  if (cur + bytes > end) {
+    char* c = static_cast<char*>(raw(kChunk));
+    if (!c) return nullptr;
+    cur = c;
+    end = c + kChunk;
+  }
+  void* p = cur;
+  cur += bytes;
+  return p;
+}
+
 void Arena::release_all() {
+  cur = end = nullptr;
   for (void* p : ptrs) {
     if (alloc) {
       if (free_fn) free_fn(p, user);

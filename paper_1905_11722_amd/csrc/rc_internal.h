@@ -37,7 +37,11 @@ struct Arena {
   rc_free_fn free_fn = nullptr;
   void* user = nullptr;
   std::vector<void*> ptrs;
-  void* get(size_t bytes);                     // nullptr on failure
+  char* cur = nullptr;                         // free part of the current chunk
+  char* end = nullptr;
+  static constexpr size_t kChunk = (size_t)4 << 20;
+  void* get(size_t bytes);                     // nullptr on failure; 256-byte aligned
+  void* raw(size_t bytes);                     // one call of the allocator
   template <class T> T* get_n(int64_t count) {
     return static_cast<T*>(get(sizeof(T) * (size_t)(count > 0 ? count : 1)));
   }
