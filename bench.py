@@ -107,6 +107,54 @@ def time_case(rcdp, torch, case, steps, warmup):
     }
 
 
+def mc_sweep(rcdp, torch, name="resnet50", count=32, reps=2):
+    """The memory-centric sweep of the ResNet-50-shaped graph: the smallest
+    feasible budget (rc_min_budget), then `count` budgets from it to 2 M(V),
+    solved in one batched fill (rc_solve_batch) and each traced; the same
+    budgets solved one by one are timed beside it."""
+    case = workloads_case(name)
+    g = rcdp.Graph.create(case.graph)
+    fam = g.build_family(case.mode)
+    top = 2 * sum(case.graph.M)
+    best = None
+    for _ in range(reps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        b_min = fam.min_budget()
+        t1 = time.perf_counter()
+        budgets = [b_min + (j * (top - b_min)) // (count - 1) for j in range(count)]
+        sols = fam.sweep(budgets, "mc")
+        for _, sol in sols:
+            sol.reconstruct()
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        t_mc = [sol.t_star for _, sol in sols]
+        batch_fill = sols[0][1].fill_ms()
+        for _, sol in sols:
+            sol.free()
+        t3 = time.perf_counter()
+        for B in budgets:
+            sol = fam.solve(B, "mc")
+            sol.reconstruct()
+            sol.free()
+        torch.cuda.synchronize()
+        t4 = time.perf_counter()
+        res = {"workload": name, "budgets": count, "B_min": b_min, "B_max": top,
+               "min_budget_ms": (t1 - t0) * 1e3, "batched_sweep_ms": (t2 - t1) * 1e3,
+               "batched_fill_ms": batch_fill, "one_by_one_ms": (t4 - t3) * 1e3,
+               "t_mc_first_last": [t_mc[0], t_mc[-1]]}
+        if best is None or res["batched_sweep_ms"] < best["batched_sweep_ms"]:
+            best = res
+    fam.free()
+    g.free()
+    return best
+
+
+def workloads_case(name):
+    from paper_1905_11722_amd import workloads
+    return workloads.case(name)
+
+
 def cpu_baseline(case, relaxations):
     from oracle import oracle
     t0 = time.perf_counter()
@@ -191,6 +239,8 @@ def main():
                 "k": r["k"],
             }
 
+    sweep = None if args.no_other_graphs else mc_sweep(rcdp, torch)
+
     out = {
         "metric": "DP cell relaxations/sec (whole step: family + fill + traceback)",
         "value": W / step_s,
@@ -239,6 +289,7 @@ def main():
             "frac_of_int32_peak": achieved / VALU_INT32_PEAK_TOPS,
         },
         "per_graph": per_graph,
+        "mc_sweep": sweep,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(case, W)

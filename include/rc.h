@@ -161,6 +161,23 @@ void rc_family_free(rc_family f);
  */
 int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solution* out,
              int64_t* t_opt, int64_t* m_opt);
+/*
+ * rc_solve_batch -- rc_solve at nb budgets of one family in one pass: the
+ * memory-centric sweep of Section 4.4 solves the same family at a range of
+ * budgets.  The tables are filled together (for wide tables one launch of
+ * the wavefront kernel hands out the columns of all nb tables), then each
+ * is selected as rc_solve would.
+ *  B_host[nb]: budgets (>= 0).  out_host[nb]: one solution handle per
+ *  budget, each freed with rc_solution_free.  t_opt[nb], m_opt[nb] (may be
+ *  NULL): as rc_solve, -1 where infeasible.
+ *  rc_solution_fill_ms / rc_solution_fill_kernel_ms of every handle report
+ *  the time of the whole batched fill.
+ * Returns RC_OK (every budget solved, feasible or not), or an error as
+ * rc_solve (then no handle is created): RC_E_ARG (NULL, nb <= 0, a negative
+ * budget, bad objective), RC_E_OVERFLOW, RC_E_NOMEM, RC_E_DEVICE.
+ */
+int rc_solve_batch(rc_family f, const int64_t* B_host, int32_t nb, int32_t objective,
+                   void* stream, rc_solution* out_host, int64_t* t_opt, int64_t* m_opt);
 /* Milliseconds between HIP events recorded on the solve's stream just
  * before the first and just after the last DP-fill kernel of the solve. */
 int rc_solution_fill_ms(rc_solution s, float* ms);

@@ -89,25 +89,7 @@ struct Geo {
   static_assert(NI * (D - 1) < 63, "vmcnt range");
 };
 
-struct BParams {
-  int32_t F;
-  int32_t nblk;
-  int32_t K;                             // columns
-  const int32_t* w;
-  const int64_t* row_off;
-  const int64_t* clu_ptr;                // first compact panel record of each block
-  const int32_t* crec;
-  const int32_t* meta;                   // [nblk * kMetaInts]
-  const int32_t* push;                   // [nblk * kJB * kPushInts]
-  const int32_t* live;                   // [nblk * cap * 2] live panel records per column
-  int32_t cap;
-  const uint16_t* sentinel;              // 8 cells of infinity
-  uint16_t* m;
-  int32_t* progress;
-  int32_t* ticket;
-  DevStatus* st;
-  int64_t timeout_ticks;
-};
+
 
 // Read-only inputs of the fill, read through the constant address space so
 // that wave-uniform reads become scalar loads (they must not occupy the
@@ -171,8 +153,13 @@ __device__ __forceinline__ bool has_half(u32x4 v, uint32_t code) {
   return r;
 }
 
+// One launch fills nb tables of the same family (different budgets): the
+// ticket t takes column t / nb of table t % nb, so every table's columns are
+// still handed out right to left and a column only waits for columns with
+// smaller tickets.  nb = 1: the table of p0; else bps[0 .. nb) (device).
 template <int CPT>
-__global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p) {
+__global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p0, const BParams* bps,
+                                                           int32_t nb) {
   using G = Geo<CPT>;
   constexpr int C = G::C, D = G::D, NW = G::NW, NH = G::NH, NI = G::NI, WIN = G::WIN;
   constexpr int NCH = G::NCH, IPR = G::IPR, RB = G::RB, FB = G::FB, NCF = G::NCF, CPL = G::CPL;
@@ -194,10 +181,6 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p) {
   if (ctl) __builtin_amdgcn_s_setprio(3);
   const u16x2 kInf2 = (u16x2)((unsigned short)kInfM);
   uint32_t step = 0;
-  cint32* const meta = (cint32*)p.meta;
-  cint32* const push = (cint32*)p.push;
-  cint64* const clu_ptr = (cint64*)p.clu_ptr;
-  cint32* const live = (cint32*)p.live;
 
   auto bar = [&]() __attribute__((always_inline)) {
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
@@ -216,15 +199,21 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p) {
 
   while (true) {
     if (ctl && lane == 0) {
-      s_col = atomicAdd(p.ticket, 1);
+      s_col = atomicAdd(p0.ticket, 1);
       s_cur[0] = -1;
       s_cur[1] = 0;
       s_cur[2] = 1;                                  // the panel of block 0 may start
     }
     ctl_write();
     bar();
-    const int32_t c = __builtin_amdgcn_readfirstlane(s_col);
-    if (c >= p.K) return;
+    const int32_t tk = __builtin_amdgcn_readfirstlane(s_col);
+    if (tk >= p0.K * nb) return;
+    const int32_t c = tk / nb;
+    const BParams p = nb == 1 ? p0 : bps[tk % nb];
+    cint32* const meta = (cint32*)p.meta;
+    cint32* const push = (cint32*)p.push;
+    cint64* const clu_ptr = (cint64*)p.clu_ptr;
+    cint32* const live = (cint32*)p.live;
     ctl_write();                                   // the state the first step reads
     const int32_t u0 = -(c + 1) * C + 1;          // u of the column's first cell
     const int64_t cC = (int64_t)c * C;
@@ -652,10 +641,10 @@ __global__ void k_blocked_init(int32_t* progress, int32_t K, int32_t* ticket) {
 }
 
 template <int CPT>
-hipError_t launch_cpt(const BParams& prm, int32_t grid, hipEvent_t e0, hipEvent_t e1,
-                      hipStream_t s) {
+hipError_t launch_cpt(const BParams& prm, const BParams* bps, int32_t nb, int32_t grid,
+                      hipEvent_t e0, hipEvent_t e1, hipStream_t s) {
   if (e0 && hipEventRecord(e0, s) != hipSuccess) return hipErrorUnknown;
-  hipLaunchKernelGGL(k_fill_blocked<CPT>, dim3(grid), dim3(kThreads), 0, s, prm);
+  hipLaunchKernelGGL(k_fill_blocked<CPT>, dim3(grid), dim3(kThreads), 0, s, prm, bps, nb);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (e1 && hipEventRecord(e1, s) != hipSuccess) return hipErrorUnknown;
@@ -690,52 +679,94 @@ int64_t blocked_columns(rc_family f) {
   return (f->max_row + C - 1) / C;
 }
 
-hipError_t launch_fill_blocked(rc_solution sol, hipStream_t s) {
-  rc_family f = sol->f;
-  if (f->F < 2) return hipSuccess;
-  const int cpt = blocked_cells_per_thread(f);
-  const int32_t C = kBT * cpt;
-  const int32_t K = (int32_t)((f->max_row + C - 1) / C);
+namespace {
+
+int64_t wait_ticks() {
   int dev = 0;
   int clock_khz = 0;
   (void)hipGetDevice(&dev);
   if (hipDeviceGetAttribute(&clock_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
       clock_khz <= 0)
     clock_khz = 100000;
+  return (int64_t)clock_khz * 1000 * 4;                // 4 s per wait
+}
+
+// Per-table preparation (records, push lists, pending marks) and the kernel
+// parameters of that table.
+hipError_t prepare_table(rc_solution sol, int32_t C, int32_t K, int32_t* ticket, BParams* prm,
+                         hipStream_t s) {
+  rc_family f = sol->f;
   hipLaunchKernelGGL(k_blocked_init, dim3((K + 255) / 256), dim3(256), 0, s, sol->progress, K,
-                     sol->ticket);
+                     ticket);
   hipError_t pe = launch_fill_pending(sol, s);
   if (pe == hipSuccess) pe = launch_pad_init(sol, s);
   if (pe == hipSuccess) pe = launch_rec_prepare(sol, s);
   if (pe == hipSuccess) pe = launch_rec_sort(sol, C, s);
   if (pe == hipSuccess) pe = launch_push_prepare(sol, C, s);
   if (pe != hipSuccess) return pe;
-  BParams prm;
-  prm.F = (int32_t)f->F;
-  prm.nblk = (int32_t)f->nblk;
-  prm.K = K;
-  prm.w = f->w;
-  prm.row_off = f->row_off;
-  prm.clu_ptr = f->clu_ptr;
-  prm.crec = sol->crec;
-  prm.meta = sol->blk_meta;
-  prm.push = sol->push;
-  prm.live = sol->live;
-  prm.cap = sol->live_cap;
-  prm.sentinel = sol->sentinel;
-  prm.m = sol->m;
-  prm.progress = sol->progress;
-  prm.ticket = sol->ticket;
-  prm.st = sol->status;
-  prm.timeout_ticks = (int64_t)clock_khz * 1000 * 4;   // 4 s per wait
+  prm->F = (int32_t)f->F;
+  prm->nblk = (int32_t)f->nblk;
+  prm->K = K;
+  prm->w = f->w;
+  prm->row_off = f->row_off;
+  prm->clu_ptr = f->clu_ptr;
+  prm->crec = sol->crec;
+  prm->meta = sol->blk_meta;
+  prm->push = sol->push;
+  prm->live = sol->live;
+  prm->cap = sol->live_cap;
+  prm->sentinel = sol->sentinel;
+  prm->m = sol->m;
+  prm->progress = sol->progress;
+  prm->ticket = ticket;
+  prm->st = sol->status;
+  prm->timeout_ticks = wait_ticks();
+  return hipSuccess;
+}
+
+hipError_t launch_kernel(const BParams& prm, const BParams* bps, int32_t nb, int cpt,
+                         hipEvent_t e0, hipEvent_t e1, hipStream_t s) {
   // Any grid size is correct; more workgroups than columns would idle.
-  const int32_t grid = (int32_t)std::min<int64_t>(K, (int64_t)g_num_cus * 4);
+  const int64_t cols = (int64_t)prm.K * nb;
+  const int32_t grid = (int32_t)std::min<int64_t>(cols, (int64_t)g_num_cus * 4);
   if (std::getenv("RCDP_DEBUG"))
-    std::fprintf(stderr, "rcdp: blocked fill K=%d columns of %d cells, grid=%d, %lld blocks\n", K,
-                 C, grid, (long long)f->nblk);
-  if (cpt == 1) return launch_cpt<1>(prm, grid, sol->evk0, sol->evk1, s);
-  if (cpt == 2) return launch_cpt<2>(prm, grid, sol->evk0, sol->evk1, s);
-  return launch_cpt<4>(prm, grid, sol->evk0, sol->evk1, s);
+    std::fprintf(stderr, "rcdp: blocked fill %d table(s) x K=%d columns of %d cells, grid=%d\n",
+                 nb, prm.K, kBT * cpt, grid);
+  if (cpt == 1) return launch_cpt<1>(prm, bps, nb, grid, e0, e1, s);
+  if (cpt == 2) return launch_cpt<2>(prm, bps, nb, grid, e0, e1, s);
+  return launch_cpt<4>(prm, bps, nb, grid, e0, e1, s);
+}
+
+}  // namespace
+
+hipError_t launch_fill_blocked(rc_solution sol, hipStream_t s) {
+  rc_family f = sol->f;
+  if (f->F < 2) return hipSuccess;
+  const int cpt = blocked_cells_per_thread(f);
+  const int32_t C = kBT * cpt;
+  const int32_t K = (int32_t)((f->max_row + C - 1) / C);
+  BParams prm;
+  const hipError_t pe = prepare_table(sol, C, K, sol->ticket, &prm, s);
+  if (pe != hipSuccess) return pe;
+  return launch_kernel(prm, nullptr, 1, cpt, sol->evk0, sol->evk1, s);
+}
+
+hipError_t launch_fill_blocked_batch(rc_solution* sols, int32_t nb, BParams* host_prm,
+                                     BParams* dev_prm, hipStream_t s) {
+  rc_family f = sols[0]->f;
+  if (f->F < 2) return hipSuccess;
+  const int cpt = blocked_cells_per_thread(f);
+  const int32_t C = kBT * cpt;
+  const int32_t K = (int32_t)((f->max_row + C - 1) / C);
+  for (int32_t b = 0; b < nb; b++) {
+    // every table resets the shared ticket; they all run before the kernel
+    const hipError_t pe = prepare_table(sols[b], C, K, sols[0]->ticket, &host_prm[b], s);
+    if (pe != hipSuccess) return pe;
+  }
+  const hipError_t ce = hipMemcpyAsync(dev_prm, host_prm, sizeof(BParams) * (size_t)nb,
+                                       hipMemcpyHostToDevice, s);
+  if (ce != hipSuccess) return ce;
+  return launch_kernel(host_prm[0], dev_prm, nb, cpt, sols[0]->evk0, sols[0]->evk1, s);
 }
 
 }  // namespace rcdp

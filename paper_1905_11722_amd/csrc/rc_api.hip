@@ -480,13 +480,14 @@ static int choose_fill_path(rc_family f) {
   return (f->max_row >= 8192 && f->level_ptr.size() > 100) ? 1 : 0;
 }
 
-int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solution* out,
-             int64_t* t_opt, int64_t* m_opt) {
-  if (!f || !out || B < 0) return RC_E_ARG;
+}  // extern "C"
+
+// A solution handle with its buffers and events; nothing enqueued yet.
+static int new_solution(rc_family f, int64_t B, int32_t objective, rc_solution* out) {
+  if (!f || B < 0) return RC_E_ARG;
   if (objective != RC_TIME_CENTRIC && objective != RC_MEMORY_CENTRIC) return RC_E_ARG;
   const int64_t Beff = std::min<int64_t>(B, 2 * f->g->M_total);
   if (Beff > kMaxBudget) return RC_E_OVERFLOW;
-  hipStream_t s = as_stream(stream);
   rc_solution sol = new (std::nothrow) rc_solution_s();
   if (!sol) return RC_E_NOMEM;
   sol->f = f;
@@ -497,7 +498,6 @@ int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solutio
   sol->arena.free_fn = f->arena.free_fn;
   sol->arena.user = f->arena.user;
   auto fail = [&](int st) {
-    (void)hipStreamSynchronize(s);
     destroy_events(sol);
     sol->arena.release_all();
     delete sol;
@@ -527,18 +527,57 @@ int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solutio
     sol->push = sol->arena.get_n<int32_t>(f->nblk * kJB * kPushInts);
     sol->sentinel = sol->arena.get_n<uint16_t>(8);
     if (!sol->progress || !sol->ticket || !sol->crec || !sol->crec_tmp || !sol->live ||
-        !sol->blk_meta ||
-        !sol->push || !sol->sentinel)
+        !sol->blk_meta || !sol->push || !sol->sentinel)
       return fail(RC_E_NOMEM);
   }
+  *out = sol;
+  return RC_OK;
+}
+
+static void drop_solution(rc_solution sol) {
+  destroy_events(sol);
+  sol->arena.release_all();
+  delete sol;
+}
+
+// The selection result read back from the device, into the handle.
+static int settle_solution(rc_solution sol, const DevStatus& hs, float fill_ms, float kernel_ms) {
+  if (hs.error) {
+    set_last_error_msg(hs.error == 3 ? "blocked fill: a wait timed out (kernel aborted)"
+                                     : "DP fill kernel reported an inconsistency");
+    return RC_E_DEVICE;
+  }
+  sol->fill_ms = fill_ms;
+  sol->kernel_ms = kernel_ms;
+  sol->t_star = hs.t_sel;
+  sol->m_star = hs.t_sel >= 0 ? hs.m_sel : -1;
+  sol->result = hs.t_sel >= 0 ? RC_OK : RC_INFEASIBLE;
+  return sol->result;
+}
+
+static float elapsed(hipEvent_t a, hipEvent_t b) {
+  float ms = -1.f;
+  if (!a || !b || hipEventElapsedTime(&ms, a, b) != hipSuccess) return -1.f;
+  return ms;
+}
+
+extern "C" {
+
+int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solution* out,
+             int64_t* t_opt, int64_t* m_opt) {
+  if (!f || !out) return RC_E_ARG;
+  hipStream_t s = as_stream(stream);
+  rc_solution sol = nullptr;
+  const int st0 = new_solution(f, B, objective, &sol);
+  if (st0 != RC_OK) return st0;
+  auto fail = [&](int st) {
+    (void)hipStreamSynchronize(s);
+    drop_solution(sol);
+    return st;
+  };
   if (launch_solve_init(sol, s) != hipSuccess) return fail(RC_E_DEVICE);
   if (hipEventRecord(sol->ev0, s) != hipSuccess) return fail(RC_E_DEVICE);
-  hipError_t fe = hipSuccess;
-  if (sol->fill_path == 1) {
-    fe = launch_fill_blocked(sol, s);
-  } else {
-    fe = launch_fill(sol, s);
-  }
+  const hipError_t fe = sol->fill_path == 1 ? launch_fill_blocked(sol, s) : launch_fill(sol, s);
   if (fe != hipSuccess) {
     set_last_error(sol->fill_path == 1 ? "blocked fill launch" : "level fill launch", fe);
     return fail(RC_E_DEVICE);
@@ -549,22 +588,76 @@ int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solutio
   if (hipMemcpyAsync(&hs, sol->status, sizeof(hs), hipMemcpyDeviceToHost, s) != hipSuccess ||
       hipStreamSynchronize(s) != hipSuccess)
     return fail(RC_E_DEVICE);
-  if (hs.error) {
-    set_last_error_msg(hs.error == 3 ? "blocked fill: a wait timed out (kernel aborted)"
-                                     : "DP fill kernel reported an inconsistency");
-    return fail(RC_E_DEVICE);
-  }
-  if (hipEventElapsedTime(&sol->fill_ms, sol->ev0, sol->ev1) != hipSuccess) sol->fill_ms = -1.f;
-  sol->kernel_ms = sol->fill_ms;
-  if (sol->evk0 && hipEventElapsedTime(&sol->kernel_ms, sol->evk0, sol->evk1) != hipSuccess)
-    sol->kernel_ms = -1.f;
-  sol->t_star = hs.t_sel;
-  sol->m_star = hs.t_sel >= 0 ? hs.m_sel : -1;
-  sol->result = hs.t_sel >= 0 ? RC_OK : RC_INFEASIBLE;
+  const float fill_ms = elapsed(sol->ev0, sol->ev1);
+  const float kernel_ms = sol->evk0 ? elapsed(sol->evk0, sol->evk1) : fill_ms;
+  const int st = settle_solution(sol, hs, fill_ms, kernel_ms);
+  if (st < 0) return fail(st);
   if (t_opt) *t_opt = sol->t_star;
   if (m_opt) *m_opt = sol->m_star;
   *out = sol;
-  return sol->result;
+  return st;
+}
+
+int rc_solve_batch(rc_family f, const int64_t* B_host, int32_t nb, int32_t objective,
+                   void* stream, rc_solution* out_host, int64_t* t_opt, int64_t* m_opt) {
+  if (!f || !B_host || !out_host || nb <= 0) return RC_E_ARG;
+  hipStream_t s = as_stream(stream);
+  std::vector<rc_solution> sols;
+  auto fail = [&](int st) {
+    (void)hipStreamSynchronize(s);
+    for (rc_solution x : sols) drop_solution(x);
+    return st;
+  };
+  for (int32_t b = 0; b < nb; b++) {
+    rc_solution x = nullptr;
+    const int st = new_solution(f, B_host[b], objective, &x);
+    if (st != RC_OK) return fail(st);
+    sols.push_back(x);
+  }
+  for (rc_solution x : sols)
+    if (launch_solve_init(x, s) != hipSuccess) return fail(RC_E_DEVICE);
+  rc_solution s0 = sols[0];
+  if (hipEventRecord(s0->ev0, s) != hipSuccess) return fail(RC_E_DEVICE);
+  std::vector<BParams> host_prm;
+  if (s0->fill_path == 1) {
+    host_prm.resize((size_t)nb);
+    BParams* dev_prm = s0->arena.get_n<BParams>(nb);
+    if (!dev_prm) return fail(RC_E_NOMEM);
+    const hipError_t fe = launch_fill_blocked_batch(sols.data(), nb, host_prm.data(), dev_prm, s);
+    if (fe != hipSuccess) {
+      set_last_error("batched blocked fill launch", fe);
+      return fail(RC_E_DEVICE);
+    }
+  } else {
+    for (rc_solution x : sols) {
+      const hipError_t fe = launch_fill(x, s);
+      if (fe != hipSuccess) {
+        set_last_error("level fill launch", fe);
+        return fail(RC_E_DEVICE);
+      }
+    }
+  }
+  if (hipEventRecord(s0->ev1, s) != hipSuccess) return fail(RC_E_DEVICE);
+  for (rc_solution x : sols)
+    if (launch_select(x, s) != hipSuccess) return fail(RC_E_DEVICE);
+  std::vector<DevStatus> hs((size_t)nb);
+  for (int32_t b = 0; b < nb; b++)
+    if (hipMemcpyAsync(&hs[b], sols[b]->status, sizeof(DevStatus), hipMemcpyDeviceToHost, s) !=
+        hipSuccess)
+      return fail(RC_E_DEVICE);
+  if (hipStreamSynchronize(s) != hipSuccess) return fail(RC_E_DEVICE);
+  const float fill_ms = elapsed(s0->ev0, s0->ev1);
+  const float kernel_ms = s0->evk0 ? elapsed(s0->evk0, s0->evk1) : fill_ms;
+  for (int32_t b = 0; b < nb; b++) {
+    const int st = settle_solution(sols[b], hs[b], fill_ms, kernel_ms);
+    if (st < 0) return fail(st);
+  }
+  for (int32_t b = 0; b < nb; b++) {
+    out_host[b] = sols[b];
+    if (t_opt) t_opt[b] = sols[b]->t_star;
+    if (m_opt) m_opt[b] = sols[b]->m_star;
+  }
+  return RC_OK;
 }
 
 int rc_solution_fill_ms(rc_solution s, float* ms) {

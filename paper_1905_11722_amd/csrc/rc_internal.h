@@ -204,6 +204,29 @@ hipError_t launch_fill_pending(rc_solution sol, hipStream_t s);
 hipError_t launch_pad_init(rc_solution sol, hipStream_t s);
 int blocked_cells_per_thread(rc_family f);
 
+// Kernel parameters of one table of the blocked fill (blocked.hip).
+struct BParams {
+  int32_t F;
+  int32_t nblk;
+  int32_t K;                             // columns
+  const int32_t* w;
+  const int64_t* row_off;
+  const int64_t* clu_ptr;                // first compact panel record of each block
+  const int32_t* crec;
+  const int32_t* meta;                   // [nblk * kMetaInts]
+  const int32_t* push;                   // [nblk * kJB * kPushInts]
+  const int32_t* live;                   // [nblk * cap * 2] live panel records per column
+  int32_t cap;
+  const uint16_t* sentinel;              // 8 cells of infinity
+  uint16_t* m;
+  int32_t* progress;
+  int32_t* ticket;
+  DevStatus* st;
+  int64_t timeout_ticks;
+};
+hipError_t launch_fill_blocked_batch(rc_solution* sols, int32_t nb, BParams* host_prm,
+                                     BParams* dev_prm, hipStream_t s);
+
 // ---- smallest feasible budget (budget.hip)
 size_t min_budget_scratch_bytes(rc_family f, int32_t hi0);
 hipError_t launch_min_budget(rc_family f, int32_t hi0, uint32_t* scratch, hipStream_t s);

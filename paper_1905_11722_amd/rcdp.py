@@ -87,6 +87,10 @@ def load_library():
     lib.rc_solve.argtypes = [P, i64, i32, P, pp, ctypes.POINTER(i64), ctypes.POINTER(i64)]
     lib.rc_solution_fill_ms.restype = ctypes.c_int
     lib.rc_solution_fill_ms.argtypes = [P, ctypes.POINTER(ctypes.c_float)]
+    lib.rc_solve_batch.restype = ctypes.c_int
+    lib.rc_solve_batch.argtypes = [P, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                   ctypes.c_void_p]
     lib.rc_min_budget.restype = ctypes.c_int
     lib.rc_min_budget.argtypes = [P, ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64)]
     lib.rc_solution_fill_kernel_ms.restype = ctypes.c_int
@@ -241,9 +245,22 @@ class Family:
         return b.value
 
     def sweep(self, budgets, objective="mc"):
-        """Solve at each budget in turn: [(budget, Solution)].  The memory-centric
-        sweep of Section 4.4 runs the same family at a range of budgets."""
-        return [(int(B), self.solve(int(B), objective)) for B in budgets]
+        """Solve at every budget in one batched fill (rc_solve_batch):
+        [(budget, Solution)].  The memory-centric sweep of Section 4.4 runs the
+        same family at a range of budgets."""
+        lib = load_library()
+        Bs = np.asarray([int(B) for B in budgets], dtype=np.int64)
+        nb = len(Bs)
+        hs = (ctypes.c_void_p * nb)()
+        t = np.full(nb, -1, dtype=np.int64)
+        m = np.full(nb, -1, dtype=np.int64)
+        st = lib.rc_solve_batch(self._h, Bs.ctypes.data, nb, OBJECTIVES.get(objective, objective),
+                                _stream(), ctypes.cast(hs, ctypes.c_void_p), t.ctypes.data,
+                                m.ctypes.data)
+        _check(st, "rc_solve_batch")
+        return [(int(Bs[b]), Solution(ctypes.c_void_p(hs[b]), self,
+                                      OK if t[b] >= 0 else INFEASIBLE, int(t[b]), int(m[b])))
+                for b in range(nb)]
 
     def solve(self, B, objective="tc"):
         lib = load_library()

@@ -327,3 +327,27 @@ def test_paper_cost_convention(rc, oracle_mod, name):
     compare(rc, oracle_mod, c.graph, c.mode, c.B)
     fam = rc.Graph.create(c.graph).build_family(c.mode)
     compare(rc, oracle_mod, c.graph, c.mode, fam.min_budget())
+
+
+@pytest.mark.parametrize("path", ["level", "wavefront"])
+@pytest.mark.parametrize("n,p,seed", WIDE[2::5])
+def test_solve_batch_tables(rc, oracle_mod, monkeypatch, path, n, p, seed):
+    """rc_solve_batch: every budget's table, t* and schedule as the oracle's,
+    the tables of all budgets filled in one pass."""
+    monkeypatch.setenv("RCDP_FILL", path)
+    g = W.random_dag(n, p, 5000 + seed, tmax=700, mmax=60)
+    lo, hi = 2 * max(g.M), 2 * sum(g.M)
+    budgets = [lo, (3 * lo + hi) // 4, (lo + hi) // 2, hi, lo - 1]
+    for mode in ("exact", "pruned"):
+        fam = rc.Graph.create(g).build_family(mode)
+        for objective in ("tc", "mc"):
+            for B, sol in fam.sweep(budgets, objective):
+                ref = oracle_mod.solve(g, mode, max(B, 0), objective)
+                assert (sol.t_star, sol.m_star) == (ref.t_star, ref.m_star), (B, mode, objective)
+                m, _ = sol.table()
+                rm, _ = ref.table()
+                np.testing.assert_array_equal(m, rm)
+                if ref.status == oracle_mod.OK:
+                    chain, _, _ = ref.schedule()
+                    np.testing.assert_array_equal(sol.reconstruct().chain, chain)
+                sol.free()
