@@ -130,7 +130,14 @@ __device__ __forceinline__ void wait_vm() {
 
 __device__ __forceinline__ void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
-__device__ __forceinline__ int32_t ld_relaxed(const int32_t* p) {
+// Global-memory pointers: the parameters of a batched launch come from
+// memory, where the compiler no longer sees that they point to global
+// memory; flat accesses would also count against the LDS counter that every
+// step's barrier waits on.
+typedef __attribute__((address_space(1))) int32_t gint32;
+typedef __attribute__((address_space(1))) DevStatus gstatus;
+
+__device__ __forceinline__ int32_t ld_relaxed(const gint32* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -209,7 +216,20 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p0, const BPa
     const int32_t tk = __builtin_amdgcn_readfirstlane(s_col);
     if (tk >= p0.K * nb) return;
     const int32_t c = tk / nb;
-    const BParams p = nb == 1 ? p0 : bps[tk % nb];
+    // the batch's parameters are read through the constant address space, so
+    // that they load into scalar registers like the kernel arguments
+    BParams p = p0;
+    if (nb != 1) {
+      typedef const __attribute__((address_space(4))) uint64_t cu64;
+      static_assert(sizeof(BParams) % 8 == 0, "parameter words");
+      struct Words { uint64_t v[sizeof(BParams) / 8]; } wd;
+      cu64* const q = (cu64*)(bps + tk % nb);
+#pragma unroll
+      for (int i = 0; i < (int)(sizeof(BParams) / 8); i++) wd.v[i] = q[i];
+      p = __builtin_bit_cast(BParams, wd);
+    }
+    gint32* const progress = (gint32*)p.progress;
+    gstatus* const gst = (gstatus*)p.st;
     cint32* const meta = (cint32*)p.meta;
     cint32* const push = (cint32*)p.push;
     cint64* const clu_ptr = (cint64*)p.clu_ptr;
@@ -403,7 +423,7 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p0, const BPa
       bool ok = true;
       for (int32_t d0 = 0; d0 <= poll_reach && ok; d0 += kWave) {
         const int32_t d = d0 + lane;
-        ok = __all(d > poll_reach || ld_relaxed(&p.progress[c - d]) >= poll_need);
+        ok = __all(d > poll_reach || ld_relaxed(&progress[c - d]) >= poll_need);
       }
       if (ok)
         cur_set(2, pb + 1);
@@ -431,7 +451,7 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p0, const BPa
     auto no_work = []() {};
     auto fail = [&]() {
       wait_vm<0>();                                // no DMA may land after the exit
-      if (ctl && lane == 0) p.st->error = 3;
+      if (ctl && lane == 0) gst->error = 3;
     };
 
     // ---------------- the panel of block 0 (source: the empty set's row)
@@ -618,7 +638,7 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p0, const BPa
       auto publish = [&]() __attribute__((always_inline)) {
         wait_vm<0>();
         if (lane == 0)
-          __hip_atomic_store(&p.progress[c], (int32_t)(j0 + nrows), __ATOMIC_RELAXED,
+          __hip_atomic_store(&progress[c], (int32_t)(j0 + nrows), __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_AGENT);
         cur_set(0, -1);
       };
