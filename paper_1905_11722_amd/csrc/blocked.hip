@@ -54,21 +54,18 @@
 #include <cstdlib>
 
 #include "rc_internal.h"
+#include "wavefront.h"
 
 namespace rcdp {
 
 namespace {
 
-constexpr int kWave = 64;
+using namespace wf;
+
 constexpr int kCW = 4;                   // compute waves
 constexpr int kBT = kCW * kWave;         // compute threads
 constexpr int kThreads = kBT + kWave;    // plus the control wave
-constexpr int kNB = 8;                   // panel records per pipeline stage
 constexpr uint32_t kUnset = 0xFFFD;      // LDS cell whose staging load has not landed
-
-typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
-typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 template <int CPT>
 struct Geo {
@@ -90,67 +87,6 @@ struct Geo {
 };
 
 
-
-// Read-only inputs of the fill, read through the constant address space so
-// that wave-uniform reads become scalar loads (they must not occupy the
-// vector memory counter of the compute waves).
-typedef const __attribute__((address_space(4))) int32_t cint32;
-typedef const __attribute__((address_space(4))) int64_t cint64;
-
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
-
-// 16 bytes per lane, global -> LDS at lds + 16 * lane, agent-coherent.  The
-// load is invisible to the compiler's counter bookkeeping; every wait on it
-// is explicit.
-// M0 (the LDS base of the copy) is saved and restored around it.
-__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
-  uint32_t keep;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, off sc1\n\ts_mov_b32 m0, %0"
-      : "=&s"(keep)
-      : "v"(g), "s"(lds)
-      : "memory");
-}
-
-__device__ __forceinline__ void st_sc1(void* g, u32x2 v) {
-  asm volatile("global_store_dwordx2 %0, %1, off sc1" : : "v"(g), "v"(v) : "memory");
-}
-
-__device__ __forceinline__ void st_sc1(void* g, u32x4 v) {
-  asm volatile("global_store_dwordx4 %0, %1, off sc1" : : "v"(g), "v"(v) : "memory");
-}
-
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
-}
-
-__device__ __forceinline__ void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
-
-// Global-memory pointers: the parameters of a batched launch come from
-// memory, where the compiler no longer sees that they point to global
-// memory; flat accesses would also count against the LDS counter that every
-// step's barrier waits on.
-typedef __attribute__((address_space(1))) int32_t gint32;
-typedef __attribute__((address_space(1))) DevStatus gstatus;
-
-__device__ __forceinline__ int32_t ld_relaxed(const gint32* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__device__ __forceinline__ u16x2 as_u16x2(int32_t v) { return __builtin_bit_cast(u16x2, v); }
-
-// Two relaxations of Algorithm 1 (see the header comment).
-__device__ __forceinline__ u16x2 relax2(u16x2 acc, u16x2 x, u16x2 tau, u16x2 dm) {
-  const u16x2 y = __builtin_elementwise_add_sat(x, dm);
-  const u16x2 q = __builtin_elementwise_sub_sat(x, tau);
-  u16x2 r;
-  asm("v_pk_mad_u16 %0, %1, -1, %2 clamp" : "=v"(r) : "v"(q), "v"(y));
-  return __builtin_elementwise_min(acc, r);
-}
 
 // Does a chunk of 8 staged cells hold kUnset (not landed) / kPendM?
 __device__ __forceinline__ bool has_half(u32x4 v, uint32_t code) {
@@ -216,18 +152,7 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p0, const BPa
     const int32_t tk = __builtin_amdgcn_readfirstlane(s_col);
     if (tk >= p0.K * nb) return;
     const int32_t c = tk / nb;
-    // the batch's parameters are read through the constant address space, so
-    // that they load into scalar registers like the kernel arguments
-    BParams p = p0;
-    if (nb != 1) {
-      typedef const __attribute__((address_space(4))) uint64_t cu64;
-      static_assert(sizeof(BParams) % 8 == 0, "parameter words");
-      struct Words { uint64_t v[sizeof(BParams) / 8]; } wd;
-      cu64* const q = (cu64*)(bps + tk % nb);
-#pragma unroll
-      for (int i = 0; i < (int)(sizeof(BParams) / 8); i++) wd.v[i] = q[i];
-      p = __builtin_bit_cast(BParams, wd);
-    }
+    const BParams p = batch_params(p0, bps, nb, tk);
     gint32* const progress = (gint32*)p.progress;
     gstatus* const gst = (gstatus*)p.st;
     cint32* const meta = (cint32*)p.meta;
@@ -671,9 +596,21 @@ hipError_t launch_cpt(const BParams& prm, const BParams* bps, int32_t nb, int32_
   return hipSuccess;
 }
 
-int g_num_cus = -1;
-
 }  // namespace
+
+int num_cus() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] <= 0) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        v <= 0)
+      v = 256;
+    cached[dev] = v;
+  }
+  return cached[dev];
+}
 
 // Column width: 256, 512 or 1024 cells (1, 2 or 4 cells per compute lane).
 // A column's time is dominated by its sequence of steps (one per panel stage
@@ -682,16 +619,10 @@ int g_num_cus = -1;
 // (more columns than about eight workgroups per CU could take) use wider
 // columns.
 int blocked_cells_per_thread(rc_family f) {
-  if (g_num_cus < 0) {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&g_num_cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-      g_num_cus = 256;
-  }
   const char* env = std::getenv("RCDP_CPT");
   if (env && (env[0] == '1' || env[0] == '2' || env[0] == '4')) return env[0] - '0';
   const int64_t k1 = (f->max_row + kBT - 1) / kBT;
-  return k1 <= 8 * (int64_t)g_num_cus ? 1 : 4;
+  return k1 <= 8 * (int64_t)num_cus() ? 1 : 4;
 }
 
 int64_t blocked_columns(rc_family f) {
@@ -721,7 +652,7 @@ hipError_t prepare_table(rc_solution sol, int32_t C, int32_t K, int32_t* ticket,
   hipError_t pe = launch_fill_pending(sol, s);
   if (pe == hipSuccess) pe = launch_pad_init(sol, s);
   if (pe == hipSuccess) pe = launch_rec_prepare(sol, s);
-  if (pe == hipSuccess) pe = launch_rec_sort(sol, C, s);
+  if (pe == hipSuccess) pe = launch_rec_sort(sol, C, 0, s);
   if (pe == hipSuccess) pe = launch_push_prepare(sol, C, s);
   if (pe != hipSuccess) return pe;
   prm->F = (int32_t)f->F;
@@ -748,7 +679,7 @@ hipError_t launch_kernel(const BParams& prm, const BParams* bps, int32_t nb, int
                          hipEvent_t e0, hipEvent_t e1, hipStream_t s) {
   // Any grid size is correct; more workgroups than columns would idle.
   const int64_t cols = (int64_t)prm.K * nb;
-  const int32_t grid = (int32_t)std::min<int64_t>(cols, (int64_t)g_num_cus * 4);
+  const int32_t grid = (int32_t)std::min<int64_t>(cols, (int64_t)num_cus() * 4);
   if (std::getenv("RCDP_DEBUG"))
     std::fprintf(stderr, "rcdp: blocked fill %d table(s) x K=%d columns of %d cells, grid=%d\n",
                  nb, prm.K, kBT * cpt, grid);

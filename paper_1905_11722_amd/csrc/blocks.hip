@@ -1,7 +1,10 @@
 // Target-block records for the blocked wavefront fill (blocked.hip).
 //
-// Targets 1..F-1 (family order) are cut into blocks of kJB consecutive
-// targets.  For block b = [j0, j1) the pairs (L_i, L_j) with j in the
+// Targets 1..F-1 (family order) are cut into blocks of at most kJB
+// consecutive targets, block b = [bstart[b], bstart[b + 1]): kJB targets
+// each for the row-push wavefront (blocked.hip), blocks whose in-block
+// dependencies fit the recomputed halo for the ghost-zone wavefront
+// (ghost.hip).  For block b = [j0, j1) the pairs (L_i, L_j) with j in the
 // block split into
 //  - panel pairs, i < j0: grouped into one record per source i (ascending
 //    i), holding kJB slots (one per target of the block; e = -1 when the
@@ -26,12 +29,12 @@ namespace rcdp {
 namespace {
 
 // Number of panel sources (distinct i < j0 over the block's pred lists).
-__global__ __launch_bounds__(256) void k_blk_count(int64_t F, const int64_t* pred_ptr,
+__global__ __launch_bounds__(256) void k_blk_count(const int32_t* bstart, const int64_t* pred_ptr,
                                                    const int32_t* pidx, int64_t* count) {
   __shared__ uint32_t bitmap[(kMaxSets + 32) / 32];
   __shared__ int32_t total;
   const int64_t b = blockIdx.x;
-  const int64_t j0 = 1 + b * kJB, j1 = j0 + kJB < F ? j0 + kJB : F;
+  const int64_t j0 = bstart[b], j1 = bstart[b + 1];
   const int words = (int)((j0 + 31) / 32);
   for (int x = threadIdx.x; x < words; x += blockDim.x) bitmap[x] = 0;
   if (threadIdx.x == 0) total = 0;
@@ -49,7 +52,7 @@ __global__ __launch_bounds__(256) void k_blk_count(int64_t F, const int64_t* pre
   if (threadIdx.x == 0) count[b] = total;
 }
 
-__global__ __launch_bounds__(256) void k_blk_fill(int64_t F, const int32_t* w,
+__global__ __launch_bounds__(256) void k_blk_fill(const int32_t* bstart, const int32_t* w,
                                                   const int64_t* pred_ptr, const int32_t* pidx,
                                                   const int32_t* pdt, const int32_t* pdm,
                                                   const int32_t* pc, const int64_t* rec_ptr,
@@ -57,7 +60,7 @@ __global__ __launch_bounds__(256) void k_blk_fill(int64_t F, const int32_t* w,
   __shared__ uint32_t bitmap[(kMaxSets + 32) / 32];
   __shared__ int32_t prefix[(kMaxSets + 32) / 32];
   const int64_t b = blockIdx.x;
-  const int64_t j0 = 1 + b * kJB, j1 = j0 + kJB < F ? j0 + kJB : F;
+  const int64_t j0 = bstart[b], j1 = bstart[b + 1];
   const int words = (int)((j0 + 31) / 32);
   const int64_t base = rec_ptr[b], nrec = rec_ptr[b + 1] - base;
   for (int x = threadIdx.x; x < words; x += blockDim.x) bitmap[x] = 0;
@@ -116,13 +119,13 @@ __global__ __launch_bounds__(256) void k_blk_fill(int64_t F, const int32_t* w,
 }  // namespace
 
 hipError_t launch_blk_count(rc_family f, int64_t nblk, int64_t* count, hipStream_t s) {
-  hipLaunchKernelGGL(k_blk_count, dim3((unsigned)nblk), dim3(256), 0, s, f->F, f->pred_ptr,
+  hipLaunchKernelGGL(k_blk_count, dim3((unsigned)nblk), dim3(256), 0, s, f->bstart, f->pred_ptr,
                      f->pidx, count);
   return hipGetLastError();
 }
 
 hipError_t launch_blk_fill(rc_family f, int64_t nblk, hipStream_t s) {
-  hipLaunchKernelGGL(k_blk_fill, dim3((unsigned)nblk), dim3(256), 0, s, f->F, f->w, f->pred_ptr,
+  hipLaunchKernelGGL(k_blk_fill, dim3((unsigned)nblk), dim3(256), 0, s, f->bstart, f->w, f->pred_ptr,
                      f->pidx, f->pdt, f->pdm, f->pc, f->rec_ptr, f->rec);
   return hipGetLastError();
 }
@@ -183,8 +186,9 @@ __global__ __launch_bounds__(256) void k_blk_clusters(const int64_t* rec_ptr, Bl
 
 // Per solve, panel records: keep the slots whose budget test can pass
 // (pair exists and B - c >= 0) of the records whose source lies before the
-// previous block (sources i < max(j0 - kJB, 1); the previous block's rows
-// reach the block through row pushes instead), and emit one compact record
+// previous block (row-push fill: sources i < bstart[b - 1], the previous
+// block's rows reach the block through row pushes instead) or before the
+// block itself (ghost-zone fill: every source i < j0), and emit one compact record
 // per shift cluster that has such a slot, compacted from clu_ptr[b] on.  A
 // compact record is kRecInts int32: [0] source i, [1] smallest shift emin,
 // [2] staged span emax - emin (<= kSpan), [3] P_i = w_i - 1, [4..5] index of
@@ -195,8 +199,12 @@ __global__ __launch_bounds__(256) void k_blk_clusters(const int64_t* rec_ptr, Bl
 // additions dm of slots 2p, 2p+1 as two uint16.  A slot without a live pair
 // gets budget 0 and addition 0xFFFF, so its candidate always saturates to
 // infinity.  meta[b * kMetaInts] = {records, largest live shift, rows of
-// the block, largest P of its rows, ...}.
-__global__ __launch_bounds__(256) void k_rec_prepare(int64_t F, int32_t Beff, const int32_t* w,
+// the block, largest P of its rows, (set by k_rec_sort), largest live
+// shift of the new group, 0, 0}; with ghost set, [1] covers the records of
+// sources before the previous block (the old group) and [5] those of the
+// previous block's rows (the new group).
+__global__ __launch_bounds__(256) void k_rec_prepare(const int32_t* bstart, int32_t ghost,
+                                                     int32_t Beff, const int32_t* w,
                                                      const int64_t* row_off,
                                                      const int64_t* rec_ptr,
                                                      const int64_t* clu_ptr, BlockRecords R,
@@ -204,14 +212,16 @@ __global__ __launch_bounds__(256) void k_rec_prepare(int64_t F, int32_t Beff, co
   const int64_t b = blockIdx.x;
   const int64_t base = rec_ptr[b], n = rec_ptr[b + 1] - base;
   const int64_t obase = clu_ptr[b];
-  const int64_t j0 = 1 + b * kJB;
-  const int64_t old_end = j0 - kJB > 1 ? j0 - kJB : 1;
+  const int64_t j0 = bstart[b];
+  const int64_t prev = b > 0 ? bstart[b - 1] : 0;    // first row of the previous block
+  const int64_t old_end = ghost ? j0 : (prev > 1 ? prev : 1);
   const int lane = threadIdx.x & 63, wave = threadIdx.x / 64;
   __shared__ int32_t s_wcnt[4];
-  __shared__ int32_t s_run, s_emax;
+  __shared__ int32_t s_run, s_emax, s_emax_new;
   if (threadIdx.x == 0) {
     s_run = 0;
     s_emax = 0;
+    s_emax_new = 0;
   }
   __syncthreads();
   for (int64_t r0 = 0; r0 < n; r0 += 256) {
@@ -270,7 +280,7 @@ __global__ __launch_bounds__(256) void k_rec_prepare(int64_t F, int32_t Beff, co
         d[20 + x] = (int32_t)dm2[x];
       }
       for (int x = 24; x < kRecInts; x++) d[x] = 0;
-      atomicMax(&s_emax, emax);
+      atomicMax(ghost && i >= prev ? &s_emax_new : &s_emax, emax);
       o++;
     }
     __syncthreads();
@@ -282,15 +292,17 @@ __global__ __launch_bounds__(256) void k_rec_prepare(int64_t F, int32_t Beff, co
     __syncthreads();
   }
   if (threadIdx.x == 0) {
-    const int64_t j1 = j0 + kJB < F ? j0 + kJB : F;
+    const int64_t j1 = bstart[b + 1];
     int32_t mp = -1;
     for (int64_t j = j0; j < j1; j++) mp = max(mp, w[j] - 1);
     int32_t* mt = meta + b * kMetaInts;
     mt[0] = s_run;                      // live panel records
-    mt[1] = s_emax;                     // largest live panel shift
+    mt[1] = s_emax;                     // largest live panel shift (old group)
     mt[2] = (int32_t)(j1 - j0);         // rows of the block
     mt[3] = mp;                         // largest P of the block's rows
-    for (int x = 4; x < kMetaInts; x++) mt[x] = 0;
+    mt[4] = 0;
+    mt[5] = s_emax_new;                 // largest live shift of the new group
+    for (int x = 6; x < kMetaInts; x++) mt[x] = 0;
   }
 }
 
@@ -384,30 +396,36 @@ __global__ __launch_bounds__(64) void k_push_prepare(int64_t F, int64_t nblk, in
   }
 }
 
-// Per solve, order of the panel records of each block: records whose slots
-// share one shift ("uniform", span 0) first, then the rest; within each
-// kind by descending cm = min(floor((P_i + emax) / C), cap - 1), the last
-// column whose cells the record's window reaches.  For every column x < cap
-// the live table holds, per kind, the number of records with cm >= x: a
-// prefix of the kind's records that contains every record whose window
-// reaches column x (for x = cap - 1 also columns beyond).  meta[4] = the
-// number of uniform records.
-__global__ __launch_bounds__(256) void k_rec_sort(int32_t C, int32_t cap, const int64_t* clu_ptr,
-                                                  const int32_t* src, int32_t* dst, int32_t* meta,
-                                                  int32_t* live) {
+// Per solve, order of the panel records of each block: two kinds, first
+// kind 0, then kind 1; within each kind by descending
+// cm = min(floor((P_i + emax + H) / C), cap - 1), the last column whose
+// cells the record's window reaches (a column also computes the H cells
+// to its right).  Kinds: ghost == 0, records whose slots share one shift
+// ("uniform", span 0) and the rest; ghost != 0, sources before the previous
+// block (old group) and the previous block's rows (new group).  For every
+// column x < cap the live table holds, per kind, the number of records with
+// cm >= x: a prefix of the kind's records that contains every record whose
+// window reaches column x (for x = cap - 1 also columns beyond).  meta[4] =
+// the number of kind-0 records.
+__global__ __launch_bounds__(256) void k_rec_sort(int32_t C, int32_t H, int32_t cap,
+                                                  const int32_t* bstart, int32_t ghost,
+                                                  const int64_t* clu_ptr, const int32_t* src,
+                                                  int32_t* dst, int32_t* meta, int32_t* live) {
   constexpr int kPer = 2 * kLiveCap / 256;       // bins per thread in the scan
   __shared__ int32_t bin[2 * kLiveCap];
   __shared__ int32_t s_part[256];
   const int64_t b = blockIdx.x;
   const int64_t base = clu_ptr[b];
   const int32_t n = meta[b * kMetaInts + 0];
+  const int32_t prev = b > 0 ? bstart[b - 1] : 0;
   const int tid = threadIdx.x;
   const int nb = 2 * cap;
   for (int x = tid; x < 2 * kLiveCap; x += 256) bin[x] = 0;
   __syncthreads();
   auto key_of = [&](const int32_t* rec) {
-    const int32_t cm = min((rec[3] + rec[6]) / C, cap - 1);
-    return (rec[2] != 0 ? cap : 0) + (cap - 1 - cm);
+    const int32_t cm = min((rec[3] + rec[6] + H) / C, cap - 1);
+    const bool kind1 = ghost ? rec[0] >= prev : rec[2] != 0;
+    return (kind1 ? cap : 0) + (cap - 1 - cm);
   };
   for (int32_t r = tid; r < n; r += 256) atomicAdd(&bin[key_of(src + (base + r) * kRecInts)], 1);
   __syncthreads();
@@ -478,16 +496,17 @@ __global__ void k_pad_init(int64_t F, const int32_t* w, const int64_t* row_off, 
 
 hipError_t launch_rec_prepare(rc_solution sol, hipStream_t s) {
   rc_family f = sol->f;
-  hipLaunchKernelGGL(k_rec_prepare, dim3((unsigned)f->nblk), dim3(256), 0, s, f->F,
-                     (int32_t)sol->Beff, f->w, f->row_off, f->rec_ptr, f->clu_ptr, f->rec,
-                     sol->crec_tmp, sol->blk_meta);
+  hipLaunchKernelGGL(k_rec_prepare, dim3((unsigned)f->nblk), dim3(256), 0, s, f->bstart,
+                     (int32_t)(f->blk_kind == kBlocksGhost), (int32_t)sol->Beff, f->w, f->row_off,
+                     f->rec_ptr, f->clu_ptr, f->rec, sol->crec_tmp, sol->blk_meta);
   return hipGetLastError();
 }
 
-hipError_t launch_rec_sort(rc_solution sol, int32_t C, hipStream_t s) {
+hipError_t launch_rec_sort(rc_solution sol, int32_t C, int32_t H, hipStream_t s) {
   rc_family f = sol->f;
-  hipLaunchKernelGGL(k_rec_sort, dim3((unsigned)f->nblk), dim3(256), 0, s, C, sol->live_cap,
-                     f->clu_ptr, sol->crec_tmp, sol->crec, sol->blk_meta, sol->live);
+  hipLaunchKernelGGL(k_rec_sort, dim3((unsigned)f->nblk), dim3(256), 0, s, C, H, sol->live_cap,
+                     f->bstart, (int32_t)(f->blk_kind == kBlocksGhost), f->clu_ptr, sol->crec_tmp,
+                     sol->crec, sol->blk_meta, sol->live);
   return hipGetLastError();
 }
 

@@ -231,6 +231,55 @@ void rc_graph_free(rc_graph g) {
 
 // ----------------------------------------------------------------- family
 
+// Which blocks the family's wavefront records use.  RCDP_FILL=wavefront
+// forces the row-push fill's fixed blocks and RCDP_FILL=ghost the ghost-zone
+// blocks (families of at most kGhostMaxSets sets).  Otherwise: fixed blocks
+// for families beyond that size and for wide tables of many levels (where
+// the row-push fill measured faster), ghost-zone blocks for the rest.
+// shape_known: max_row and the levels are set (after the host copies).
+static int32_t family_block_kind(rc_family f, bool shape_known) {
+  const int64_t F = f->F;
+  if (F < 2) return 0;
+  const char* env = std::getenv("RCDP_FILL");
+  if (F > kGhostMaxSets || (env && std::strcmp(env, "wavefront") == 0)) return kBlocksFixed;
+  if (env && std::strcmp(env, "ghost") == 0) return kBlocksGhost;
+  if (!shape_known) return -1;                 // decided once the table's shape is known
+  const bool wide_many = f->max_row >= 65536 && f->level_ptr.size() > 101;
+  return wide_many ? kBlocksFixed : kBlocksGhost;
+}
+
+// Block starts of the chosen kind (host).
+static void cut_blocks(rc_family f, const std::vector<int32_t>& near_h) {
+  f->bstart_host.clear();
+  if (f->blk_kind == kBlocksGhost) {
+    f->bstart_host = ghost_cut(f->F, near_h);
+    return;
+  }
+  for (int64_t j = 1; j < f->F; j += kJB) f->bstart_host.push_back((int32_t)j);
+  f->bstart_host.push_back((int32_t)f->F);
+}
+
+// Block starts to the device, then the number of panel sources per block
+// and their offsets (rec_ptr).  Uses the family arena; counts is scratch of
+// at least nblk + 1 entries.
+static int upload_blocks(rc_family f, int64_t* counts, hipStream_t s) {
+  Arena& A = f->arena;
+  f->nblk = (int64_t)f->bstart_host.size() - 1;
+  if (f->nblk <= 0) {
+    f->nblk = 0;
+    return RC_OK;
+  }
+  f->bstart = A.get_n<int32_t>(f->nblk + 1);
+  f->rec_ptr = A.get_n<int64_t>(f->nblk + 1);
+  if (!f->bstart || !f->rec_ptr) return RC_E_NOMEM;
+  if (hipMemcpyAsync(f->bstart, f->bstart_host.data(), sizeof(int32_t) * (size_t)(f->nblk + 1),
+                     hipMemcpyHostToDevice, s) != hipSuccess ||
+      launch_blk_count(f, f->nblk, counts, s) != hipSuccess ||
+      launch_scan(counts, f->rec_ptr, f->nblk, 1, s) != hipSuccess)
+    return RC_E_DEVICE;
+  return RC_OK;
+}
+
 static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
   rc_graph g = f->g;
   const int n = g->n, words = g->words;
@@ -315,13 +364,21 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
   if (!f->pidx || !f->pdt || !f->pdm || !f->pc) return RC_E_NOMEM;
   RC_HIP(launch_pair_write(f, walg_t, s));
   RC_HIP(launch_sum(walg_t, F, &f->status->walg, s));
-  // records of the blocked fill: one per (block of kJB targets, panel source)
-  f->nblk = (F - 1 + kJB - 1) / kJB;
-  if (f->nblk > 0) {
-    f->rec_ptr = A.get_n<int64_t>(f->nblk + 1);
-    if (!f->rec_ptr) return RC_E_NOMEM;
-    RC_HIP(launch_blk_count(f, f->nblk, counts, s));
-    RC_HIP(launch_scan(counts, f->rec_ptr, f->nblk, 1, s));
+  // blocks of the wavefront fills: kJB targets each for the row-push fill;
+  // for the ghost-zone fill cut on the host from the shifts of near pairs
+  f->blk_kind = family_block_kind(f, false);
+  std::vector<int32_t> near_h;
+  int32_t* near_d = nullptr;
+  if (f->blk_kind != 0 && f->blk_kind != kBlocksFixed) {
+    near_h.resize((size_t)(F * kNear));
+    near_d = tmp.get_n<int32_t>(F * kNear);
+    if (!near_d) return RC_E_NOMEM;
+    RC_HIP(launch_near_shifts(f, near_d, s));
+  }
+  if (f->blk_kind == kBlocksFixed) {
+    cut_blocks(f, near_h);
+    const int ub = upload_blocks(f, counts, s);
+    if (ub != RC_OK) return ub;
   }
 
   // ---- host copies for launch configuration
@@ -337,8 +394,36 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
   if (f->nblk > 0)
     RC_HIP(hipMemcpyAsync(&f->rec_total, f->rec_ptr + f->nblk, sizeof(int64_t),
                           hipMemcpyDeviceToHost, s));
+  if (near_d)
+    RC_HIP(hipMemcpyAsync(near_h.data(), near_d, sizeof(int32_t) * near_h.size(),
+                          hipMemcpyDeviceToHost, s));
   RC_HIP(hipStreamSynchronize(s));
   if (hs.error) return RC_E_DEVICE;
+  f->cells = f->row_off_host[F];
+  if (f->cells >= ((int64_t)1 << 40)) return RC_E_OVERFLOW;
+  f->level_ptr.clear();
+  f->level_maxw.clear();
+  f->max_row = 0;
+  for (int64_t i = 0; i < F; i++) {
+    if (i == 0 || size_h[i] != size_h[i - 1]) {
+      f->level_ptr.push_back(i);
+      f->level_maxw.push_back(0);
+    }
+    f->level_maxw.back() = std::max(f->level_maxw.back(), f->w_host[i]);
+    f->max_row = std::max<int64_t>(f->max_row, f->w_host[i]);
+  }
+  f->level_ptr.push_back(F);
+  if (near_d) {                                // kind not fixed before the host copies
+    if (f->blk_kind < 0) f->blk_kind = family_block_kind(f, true);
+    cut_blocks(f, near_h);
+    const int ub = upload_blocks(f, counts, s);
+    if (ub != RC_OK) return ub;
+    if (f->nblk > 0) {
+      RC_HIP(hipMemcpyAsync(&f->rec_total, f->rec_ptr + f->nblk, sizeof(int64_t),
+                            hipMemcpyDeviceToHost, s));
+      RC_HIP(hipStreamSynchronize(s));
+    }
+  }
   f->relax = hs.walg;
   f->has_records = false;
   if (f->nblk > 0 && f->rec_total <= kMaxRecords) {
@@ -363,20 +448,6 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
     RC_HIP(hipStreamSynchronize(s));
     f->has_records = true;
   }
-  f->cells = f->row_off_host[F];
-  if (f->cells >= ((int64_t)1 << 40)) return RC_E_OVERFLOW;
-  f->level_ptr.clear();
-  f->level_maxw.clear();
-  f->max_row = 0;
-  for (int64_t i = 0; i < F; i++) {
-    if (i == 0 || size_h[i] != size_h[i - 1]) {
-      f->level_ptr.push_back(i);
-      f->level_maxw.push_back(0);
-    }
-    f->level_maxw.back() = std::max(f->level_maxw.back(), f->w_host[i]);
-    f->max_row = std::max<int64_t>(f->max_row, f->w_host[i]);
-  }
-  f->level_ptr.push_back(F);
   return RC_OK;
 }
 
@@ -472,11 +543,14 @@ static void destroy_events(rc_solution sol) {
 
 static int choose_fill_path(rc_family f) {
   if (!f->has_records || f->F < 2) return 0;
+  const int wide = f->blk_kind == kBlocksGhost ? 2 : 1;   // the family's wavefront fill
   const char* env = std::getenv("RCDP_FILL");
   if (env && std::strcmp(env, "level") == 0) return 0;
-  if (env && std::strcmp(env, "wavefront") == 0) return 1;
-  // many sequential levels over wide rows: one persistent launch beats one
-  // launch per level; few levels over wide rows: the level launches win
+  if (env && (std::strcmp(env, "wavefront") == 0 || std::strcmp(env, "ghost") == 0)) return wide;
+  // the ghost-zone fill measured at least as fast as the level launches on
+  // every workload shape; the row-push fill only pays off on wide tables of
+  // many levels, where one persistent launch beats one launch per level
+  if (wide == 2) return 2;
   return (f->max_row >= 8192 && f->level_ptr.size() > 100) ? 1 : 0;
 }
 
@@ -513,21 +587,25 @@ static int new_solution(rc_family f, int64_t B, int32_t objective, rc_solution* 
   if (hipEventCreate(&sol->ev0) != hipSuccess || hipEventCreate(&sol->ev1) != hipSuccess)
     return fail(RC_E_DEVICE);
   sol->fill_path = choose_fill_path(f);
-  if (sol->fill_path == 1 &&
+  if (sol->fill_path != 0 &&
       (hipEventCreate(&sol->evk0) != hipSuccess || hipEventCreate(&sol->evk1) != hipSuccess))
     return fail(RC_E_DEVICE);
-  if (sol->fill_path == 1) {
-    sol->progress = sol->arena.get_n<int32_t>(blocked_columns(f));
+  if (sol->fill_path != 0) {
+    const int64_t K = sol->fill_path == 2 ? ghost_columns(f) : blocked_columns(f);
+    sol->progress = sol->arena.get_n<int32_t>(K);
     sol->ticket = sol->arena.get_n<int32_t>(1);
     sol->crec = sol->arena.get_n<int32_t>(f->clu_total * kRecInts);
     sol->crec_tmp = sol->arena.get_n<int32_t>(f->clu_total * kRecInts);
-    sol->live_cap = (int32_t)std::min<int64_t>(blocked_columns(f), kLiveCap);
+    sol->live_cap = (int32_t)std::min<int64_t>(K, kLiveCap);
     sol->live = sol->arena.get_n<int32_t>(f->nblk * sol->live_cap * 2);
     sol->blk_meta = sol->arena.get_n<int32_t>(f->nblk * kMetaInts);
-    sol->push = sol->arena.get_n<int32_t>(f->nblk * kJB * kPushInts);
+    if (sol->fill_path == 2)
+      sol->tri = sol->arena.get_n<int32_t>(f->nblk * kJB * kTriInts);
+    else
+      sol->push = sol->arena.get_n<int32_t>(f->nblk * kJB * kPushInts);
     sol->sentinel = sol->arena.get_n<uint16_t>(8);
     if (!sol->progress || !sol->ticket || !sol->crec || !sol->crec_tmp || !sol->live ||
-        !sol->blk_meta || !sol->push || !sol->sentinel)
+        !sol->blk_meta || !(sol->push || sol->tri) || !sol->sentinel)
       return fail(RC_E_NOMEM);
   }
   *out = sol;
@@ -543,8 +621,9 @@ static void drop_solution(rc_solution sol) {
 // The selection result read back from the device, into the handle.
 static int settle_solution(rc_solution sol, const DevStatus& hs, float fill_ms, float kernel_ms) {
   if (hs.error) {
-    set_last_error_msg(hs.error == 3 ? "blocked fill: a wait timed out (kernel aborted)"
-                                     : "DP fill kernel reported an inconsistency");
+    set_last_error_msg(hs.error == 3   ? "wavefront fill: a wait timed out (kernel aborted)"
+                       : hs.error == 4 ? "ghost fill: an in-block shift exceeds the halo"
+                                       : "DP fill kernel reported an inconsistency");
     return RC_E_DEVICE;
   }
   sol->fill_ms = fill_ms;
@@ -577,9 +656,14 @@ int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solutio
   };
   if (launch_solve_init(sol, s) != hipSuccess) return fail(RC_E_DEVICE);
   if (hipEventRecord(sol->ev0, s) != hipSuccess) return fail(RC_E_DEVICE);
-  const hipError_t fe = sol->fill_path == 1 ? launch_fill_blocked(sol, s) : launch_fill(sol, s);
+  const hipError_t fe = sol->fill_path == 2   ? launch_fill_ghost(sol, s)
+                        : sol->fill_path == 1 ? launch_fill_blocked(sol, s)
+                                              : launch_fill(sol, s);
   if (fe != hipSuccess) {
-    set_last_error(sol->fill_path == 1 ? "blocked fill launch" : "level fill launch", fe);
+    set_last_error(sol->fill_path == 2   ? "ghost fill launch"
+                   : sol->fill_path == 1 ? "blocked fill launch"
+                                         : "level fill launch",
+                   fe);
     return fail(RC_E_DEVICE);
   }
   if (hipEventRecord(sol->ev1, s) != hipSuccess) return fail(RC_E_DEVICE);
@@ -619,7 +703,17 @@ int rc_solve_batch(rc_family f, const int64_t* B_host, int32_t nb, int32_t objec
   rc_solution s0 = sols[0];
   if (hipEventRecord(s0->ev0, s) != hipSuccess) return fail(RC_E_DEVICE);
   std::vector<BParams> host_prm;
-  if (s0->fill_path == 1) {
+  std::vector<GParams> host_gprm;
+  if (s0->fill_path == 2) {
+    host_gprm.resize((size_t)nb);
+    GParams* dev_prm = s0->arena.get_n<GParams>(nb);
+    if (!dev_prm) return fail(RC_E_NOMEM);
+    const hipError_t fe = launch_fill_ghost_batch(sols.data(), nb, host_gprm.data(), dev_prm, s);
+    if (fe != hipSuccess) {
+      set_last_error("batched ghost fill launch", fe);
+      return fail(RC_E_DEVICE);
+    }
+  } else if (s0->fill_path == 1) {
     host_prm.resize((size_t)nb);
     BParams* dev_prm = s0->arena.get_n<BParams>(nb);
     if (!dev_prm) return fail(RC_E_NOMEM);

@@ -30,6 +30,12 @@ constexpr int kMetaInts = 8;                    // blocked fill: int32 per block
 constexpr int kLiveCap = 2048;                  // blocked fill: columns with their own live counts
 constexpr uint32_t kPendM = 0xFFFE;             // blocked fill: cell not written yet
 constexpr int64_t kMaxBudget = 0xFFFC;          // finite opt values stay below kPendM
+constexpr int kBlocksFixed = 1;                 // family blocks: kJB targets each (row pushes)
+constexpr int kBlocksGhost = 2;                 // family blocks: cut to fit the ghost halo
+constexpr int kGhostHalo = 64;                  // ghost-zone fill: cells recomputed to the right
+constexpr int kGhostMaxSets = 4096;             // ghost-zone fill: largest family it takes
+constexpr int kNear = kJB;                      // ghost cut: predecessors j-1 .. j-kNear examined
+constexpr int kTriInts = 16;                    // ghost-zone fill: int32 per (block, row) list
 
 // Device allocator with ownership tracking.
 struct Arena {
@@ -108,8 +114,11 @@ struct rc_family_s {
   // device: predecessor pairs, CSR by target
   int64_t* pred_ptr = nullptr;    // [F+1]
   int32_t *pidx = nullptr, *pdt = nullptr, *pdm = nullptr, *pc = nullptr;
-  // blocked fill: records per block of kJB targets (absent when too large)
+  // blocked fill: records per block of at most kJB targets (absent when too large)
+  int32_t blk_kind = 0;           // kBlocksFixed or kBlocksGhost (0: no records)
   int64_t nblk = 0;
+  int32_t* bstart = nullptr;      // [nblk+1] first target of each block
+  std::vector<int32_t> bstart_host;
   int64_t rec_total = 0;
   bool has_records = false;
   int64_t* rec_ptr = nullptr;     // [nblk+1]
@@ -146,9 +155,10 @@ struct rc_solution_s {
   int32_t live_cap = 0;           // blocked fill: columns of the live table (min(K, kLiveCap))
   int32_t* blk_meta = nullptr;    // blocked fill: per block metadata [nblk * kMetaInts]
   int32_t* push = nullptr;        // blocked fill: row push lists [nblk * kJB * kPushInts]
+  int32_t* tri = nullptr;         // ghost-zone fill: in-block lists [nblk * kJB * kTriInts]
   int32_t cpt = 1;                // blocked fill: cells per thread of a column
   uint16_t* sentinel = nullptr;   // 8 cells of infinity
-  int32_t fill_path = 0;          // 0 level launches, 1 blocked wavefront
+  int32_t fill_path = 0;          // 0 level launches, 1 row-push wavefront, 2 ghost-zone wavefront
   hipEvent_t ev0 = nullptr, ev1 = nullptr;    // around the whole fill
   hipEvent_t evk0 = nullptr, evk1 = nullptr;  // around the wavefront kernel alone
   float fill_ms = 0.f;
@@ -199,10 +209,11 @@ hipError_t launch_blk_fill(rc_family f, int64_t nblk, hipStream_t s);
 hipError_t launch_blk_clusters(rc_family f, int64_t* count, hipStream_t s);
 hipError_t launch_rec_prepare(rc_solution sol, hipStream_t s);
 hipError_t launch_push_prepare(rc_solution sol, int32_t C, hipStream_t s);
-hipError_t launch_rec_sort(rc_solution sol, int32_t C, hipStream_t s);
+hipError_t launch_rec_sort(rc_solution sol, int32_t C, int32_t H, hipStream_t s);
 hipError_t launch_fill_pending(rc_solution sol, hipStream_t s);
 hipError_t launch_pad_init(rc_solution sol, hipStream_t s);
 int blocked_cells_per_thread(rc_family f);
+int num_cus();                          // compute units of the current device (cached)
 
 // Kernel parameters of one table of the blocked fill (blocked.hip).
 struct BParams {
@@ -226,6 +237,37 @@ struct BParams {
 };
 hipError_t launch_fill_blocked_batch(rc_solution* sols, int32_t nb, BParams* host_prm,
                                      BParams* dev_prm, hipStream_t s);
+
+// ---- ghost-zone wavefront fill (ghost.hip)
+// Kernel parameters of one table.
+struct GParams {
+  int32_t F;
+  int32_t nblk;
+  int32_t K;                             // columns
+  const int32_t* bstart;                 // [nblk + 1]
+  const int64_t* clu_ptr;                // first compact panel record of each block
+  const int32_t* crec;
+  const int32_t* meta;                   // [nblk * kMetaInts]
+  const int32_t* tri;                    // [nblk * kJB * kTriInts]
+  const int32_t* live;                   // [nblk * cap * 2] live panel records per column
+  int32_t cap;
+  const uint16_t* sentinel;              // 8 cells of infinity
+  uint16_t* m;
+  int32_t* progress;
+  int32_t* ticket;
+  DevStatus* st;
+  int64_t timeout_ticks;
+};
+// near[j * kNear + d - 1] = right-aligned shift of the pair (L_{j-d}, L_j), -1 without one.
+hipError_t launch_near_shifts(rc_family f, int32_t* near, hipStream_t s);
+// Cut targets 1..F-1 into blocks of at most kJB whose in-block dependency
+// cones fit kGhostHalo cells (host; near from launch_near_shifts).
+std::vector<int32_t> ghost_cut(int64_t F, const std::vector<int32_t>& near);
+int ghost_cells_per_thread(rc_family f);
+int64_t ghost_columns(rc_family f);
+hipError_t launch_fill_ghost(rc_solution sol, hipStream_t s);
+hipError_t launch_fill_ghost_batch(rc_solution* sols, int32_t nb, GParams* host_prm,
+                                   GParams* dev_prm, hipStream_t s);
 
 // ---- smallest feasible budget (budget.hip)
 size_t min_budget_scratch_bytes(rc_family f, int32_t hi0);

@@ -1,0 +1,106 @@
+// Device helpers shared by the two wavefront DP fills (blocked.hip, ghost.hip).
+//
+// Both stream panel data global -> LDS with explicitly counted DMA loads,
+// publish finished table cells with agent-coherent stores, and relax two
+// 16-bit table cells per lane and instruction.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "rc_internal.h"
+
+namespace rcdp {
+namespace wf {
+
+constexpr int kWave = 64;
+constexpr int kNB = 8;                   // panel records per pipeline stage
+
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Read-only inputs of a fill, read through the constant address space so
+// that wave-uniform reads become scalar loads (they must not occupy the
+// vector memory counter of the waves that count their DMA loads).
+typedef const __attribute__((address_space(4))) int32_t cint32;
+typedef const __attribute__((address_space(4))) int64_t cint64;
+typedef const __attribute__((address_space(4))) uint64_t cu64;
+
+// Global-memory pointers: the parameters of a batched launch come from
+// memory, where the compiler no longer sees that they point to global
+// memory; flat accesses would also count against the LDS counter that every
+// barrier waits on.
+typedef __attribute__((address_space(1))) int32_t gint32;
+typedef __attribute__((address_space(1))) DevStatus gstatus;
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// 16 bytes per lane, global -> LDS at lds + 16 * lane, agent-coherent.  The
+// load is invisible to the compiler's counter bookkeeping; every wait on it
+// is explicit.  M0 (the LDS base of the copy) is saved and restored around it.
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+  uint32_t keep;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off sc1\n\ts_mov_b32 m0, %0"
+      : "=&s"(keep)
+      : "v"(g), "s"(lds)
+      : "memory");
+}
+
+__device__ __forceinline__ void st_sc1(void* g, u32x2 v) {
+  asm volatile("global_store_dwordx2 %0, %1, off sc1" : : "v"(g), "v"(v) : "memory");
+}
+
+__device__ __forceinline__ void st_sc1(void* g, u32x4 v) {
+  asm volatile("global_store_dwordx4 %0, %1, off sc1" : : "v"(g), "v"(v) : "memory");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
+__device__ __forceinline__ void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+__device__ __forceinline__ int32_t ld_relaxed(const gint32* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ u16x2 as_u16x2(int32_t v) { return __builtin_bit_cast(u16x2, v); }
+
+// Two relaxations of Algorithm 1: m' = x + dm if x <= tau (tau = B - c, the
+// budget test), else infinity, in packed unsigned 16-bit lanes with
+// saturation.  y = x +sat dm; q = x -sat tau is nonzero exactly when the
+// budget test fails, and q * 0xFFFF +sat y (one multiply-add with clamp) is
+// then 0xFFFF, else y.  Every finite value stays below 0xFFFF, so the
+// saturated value is the infinity code.
+__device__ __forceinline__ u16x2 relax2(u16x2 acc, u16x2 x, u16x2 tau, u16x2 dm) {
+  const u16x2 y = __builtin_elementwise_add_sat(x, dm);
+  const u16x2 q = __builtin_elementwise_sub_sat(x, tau);
+  u16x2 r;
+  asm("v_pk_mad_u16 %0, %1, -1, %2 clamp" : "=v"(r) : "v"(q), "v"(y));
+  return __builtin_elementwise_min(acc, r);
+}
+
+// The parameters of table tk % nb of a batched launch, read through the
+// constant address space so that they load into scalar registers like the
+// kernel arguments of a single-table launch (nb == 1: p0 itself).
+template <class P>
+__device__ __forceinline__ P batch_params(const P& p0, const P* ps, int32_t nb, int32_t tk) {
+  if (nb == 1) return p0;
+  static_assert(sizeof(P) % 8 == 0, "parameter words");
+  struct Words {
+    uint64_t v[sizeof(P) / 8];
+  } wd;
+  cu64* const q = (cu64*)(ps + tk % nb);
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(P) / 8); i++) wd.v[i] = q[i];
+  return __builtin_bit_cast(P, wd);
+}
+
+}  // namespace wf
+}  // namespace rcdp

@@ -183,15 +183,19 @@ def test_full_size_cases(rc, oracle_mod, name):
 
 
 # ---------------------------------------------------------------- fill paths
-# The library picks the persistent wavefront fill for wide tables and
-# per-level launches for narrow ones; RCDP_FILL forces either.  Rows wider
-# than one 512-cell column make the wavefront's cross-workgroup waits real.
+# The library picks a persistent wavefront fill for wide tables and
+# per-level launches for narrow ones; RCDP_FILL forces one: "level", the
+# row-push wavefront ("wavefront", fixed blocks of 8 targets) or the
+# ghost-zone wavefront ("ghost", blocks cut to fit its recomputed halo).
+# Rows wider than one column make the wavefront's cross-workgroup waits real.
+
+PATHS = ["level", "wavefront", "ghost"]
 
 WIDE = [(n, p, seed) for seed, (n, p) in enumerate(
     [(n, p) for n in (4, 6, 8, 10, 12) for p in (0.2, 0.45, 0.7)])]
 
 
-@pytest.mark.parametrize("path", ["level", "wavefront"])
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("n,p,seed", WIDE)
 def test_fill_paths_wide_rows(rc, oracle_mod, monkeypatch, path, n, p, seed):
     monkeypatch.setenv("RCDP_FILL", path)
@@ -202,7 +206,7 @@ def test_fill_paths_wide_rows(rc, oracle_mod, monkeypatch, path, n, p, seed):
             compare(rc, oracle_mod, g, mode, B)
 
 
-@pytest.mark.parametrize("path", ["level", "wavefront"])
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("name", SMALL + ["layered24"])
 def test_fill_paths_small_cases(rc, oracle_mod, monkeypatch, path, name):
     monkeypatch.setenv("RCDP_FILL", path)
@@ -225,11 +229,26 @@ def test_wavefront_column_widths(rc, oracle_mod, monkeypatch, cpt, n, p, seed):
             compare(rc, oracle_mod, g, mode, B)
 
 
+@pytest.mark.parametrize("cpt", ["1", "2"])
+@pytest.mark.parametrize("n,p,seed", WIDE[1::3])
+def test_ghost_column_widths(rc, oracle_mod, monkeypatch, cpt, n, p, seed):
+    """The ghost-zone fill at both column widths (256 and 576 owned cells
+    plus the 64 recomputed ones), with rows of many columns."""
+    monkeypatch.setenv("RCDP_FILL", "ghost")
+    monkeypatch.setenv("RCDP_GHOST_CPT", cpt)
+    g = W.random_dag(n, p, 7100 + seed, tmax=1500, mmax=60)
+    lo, hi = 2 * max(g.M), 2 * sum(g.M)
+    for B in (lo, (lo + hi) // 2, hi):
+        for mode in ("exact", "pruned"):
+            compare(rc, oracle_mod, g, mode, B)
+
+
+@pytest.mark.parametrize("path", ["wavefront", "ghost"])
 @pytest.mark.parametrize("seed", [10, 12, 16])
-def test_wavefront_repeated_solves(rc, oracle_mod, monkeypatch, seed):
+def test_wavefront_repeated_solves(rc, oracle_mod, monkeypatch, path, seed):
     """The same wide tables solved repeatedly: the persistent fill's columns
     meet in a different interleaving each time, and every table must match."""
-    monkeypatch.setenv("RCDP_FILL", "wavefront")
+    monkeypatch.setenv("RCDP_FILL", path)
     g = W.random_dag(12, 0.2, 5000 + seed, tmax=700, mmax=60)
     lo, hi = 2 * max(g.M), 2 * sum(g.M)
     for B in (lo, (2 * lo + hi) // 3, hi):
@@ -244,7 +263,7 @@ def test_wavefront_repeated_solves(rc, oracle_mod, monkeypatch, seed):
                 sol.free()
 
 
-@pytest.mark.parametrize("path", ["level", "wavefront"])
+@pytest.mark.parametrize("path", PATHS)
 def test_fill_paths_long_chain(rc, oracle_mod, monkeypatch, path):
     """A long chain: one target per level, rows of many columns."""
     monkeypatch.setenv("RCDP_FILL", path)
@@ -329,7 +348,7 @@ def test_paper_cost_convention(rc, oracle_mod, name):
     compare(rc, oracle_mod, c.graph, c.mode, fam.min_budget())
 
 
-@pytest.mark.parametrize("path", ["level", "wavefront"])
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("n,p,seed", WIDE[2::5])
 def test_solve_batch_tables(rc, oracle_mod, monkeypatch, path, n, p, seed):
     """rc_solve_batch: every budget's table, t* and schedule as the oracle's,
