@@ -149,6 +149,49 @@ __global__ __launch_bounds__(64) void k_ancestors_wave(int n, int words, int num
   for (int it = lane; it < n * words; it += kWave) anc_out[it] = anc[it];
 }
 
+// Transitive closure of the predecessor relation in one workgroup (graphs
+// whose masks fit LDS and have at most kClosureWords words): A[v] starts as
+// the direct predecessors of v; for every node k, each mask that contains k
+// absorbs A[k] (Warshall's algorithm, any order of k).  A[k] never contains
+// k in a DAG, so the bit tests of step k read values that step k does not
+// change.  One barrier per node, every (node, word) item of a step in
+// parallel; then L^v = A[v] + {v}.
+constexpr int kClosureWords = 8;
+constexpr int kClosureThreads = 1024;
+constexpr int kClosureItems = 4;        // items per thread: n * words <= 4096
+
+__global__ __launch_bounds__(kClosureThreads) void k_ancestors_closure(int n, int words,
+                                                                       const uint64_t* pred_mask,
+                                                                       uint64_t* anc_out) {
+  extern __shared__ uint64_t A[];
+  const int items = n * words;
+  for (int x = threadIdx.x; x < items; x += kClosureThreads) A[x] = pred_mask[x];
+  int vw[kClosureItems], wo[kClosureItems];          // row offset v * words and word w
+#pragma unroll
+  for (int r = 0; r < kClosureItems; r++) {
+    const int it = threadIdx.x + r * kClosureThreads;
+    const int v = it / words;
+    vw[r] = it < items ? v * words : -1;
+    wo[r] = it - v * words;
+  }
+  __syncthreads();
+  for (int k = 0; k < n; k++) {
+    const int kw = k >> 6;
+    const uint64_t kb = 1ull << (k & 63);
+    const int kr = k * words;
+#pragma unroll
+    for (int r = 0; r < kClosureItems; r++) {
+      if (vw[r] < 0) continue;
+      if (A[vw[r] + kw] & kb) A[vw[r] + wo[r]] |= A[kr + wo[r]];
+    }
+    __syncthreads();
+  }
+  for (int x = threadIdx.x; x < items; x += kClosureThreads) {
+    const int v = x / words, w = x - v * words;
+    anc_out[x] = A[x] | ((v >> 6) == w ? 1ull << (v & 63) : 0ull);
+  }
+}
+
 // Candidates of the pruned family, set-major: [0] = empty set,
 // [1 + v] = L^v, [n + 1] = V.
 __global__ void k_pruned_candidates(int n, int words, const uint64_t* anc, uint64_t* cand) {
@@ -390,6 +433,132 @@ __global__ __launch_bounds__(256) void k_set_quantities(
   }
 }
 
+// The same quantities for graphs of at most kLaneWords * 64 nodes, with the
+// nodes spread over the lanes instead of walked one by one: lane l takes
+// node 64 ww + l of every word ww, ORs its successor (then predecessor)
+// words into kLaneWords register accumulators and adds its costs; word w
+// of a union is then one wave OR reduction, a sum one wave sum.
+constexpr int kLaneWords = 8;
+
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int l) {
+  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)x, l);
+  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(x >> 32), l);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t wave_or_u64(uint64_t x) {
+  for (int off = 32; off > 0; off >>= 1) x |= __shfl_xor(x, off, kWave);
+  return x;
+}
+
+template <bool kLds>
+__global__ __launch_bounds__(256) void k_set_quantities_lanes(
+    int64_t F, int n, int words, int64_t fstride, const uint64_t* bits, const uint64_t* succ_g,
+    const uint64_t* pred_g, const int32_t* T, const int32_t* M, uint64_t* bd, int32_t* size,
+    int32_t* Tsum, int32_t* Msum, int32_t* Tbd, int32_t* Mbd, int32_t* A, int32_t* w_out) {
+  extern __shared__ uint64_t lds_nb[];
+  const uint64_t* succ = succ_g;
+  const uint64_t* pred = pred_g;
+  if (kLds) {
+    const int64_t cnt = (int64_t)n * words;
+    for (int64_t x = threadIdx.x; x < cnt; x += blockDim.x) {
+      lds_nb[x] = succ_g[x];
+      lds_nb[cnt + x] = pred_g[x];
+    }
+    __syncthreads();
+    succ = lds_nb;
+    pred = lds_nb + cnt;
+  }
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t s = blockIdx.x * (int64_t)(blockDim.x / kWave) + threadIdx.x / kWave;
+  if (s >= F) return;
+  // word w of L on lane w, and every word of L in scalars
+  const uint64_t L = lane < words ? bits[(int64_t)lane * fstride + s] : 0ull;
+  uint64_t Lw[kLaneWords];
+#pragma unroll
+  for (int w = 0; w < kLaneWords; w++) Lw[w] = w < words ? readlane_u64(L, w) : 0ull;
+
+  // delta+(L) \ L and the boundary: lane l walks nodes 64 ww + l of L
+  uint64_t acc[kLaneWords];
+#pragma unroll
+  for (int w = 0; w < kLaneWords; w++) acc[w] = 0;
+  uint64_t bdw = 0;                                   // boundary word `lane`
+  int64_t tl = 0, ml = 0, tb = 0, mb = 0;
+#pragma unroll
+  for (int ww = 0; ww < kLaneWords; ww++) {
+    if (ww >= words) break;
+    const int v = ww * 64 + lane;
+    const bool in = (Lw[ww] >> lane) & 1ull;
+    bool leaves = false;
+#pragma unroll
+    for (int w = 0; w < kLaneWords; w++) {
+      if (w >= words) break;
+      const uint64_t x = in ? succ[(int64_t)v * words + w] & ~Lw[w] : 0ull;
+      acc[w] |= x;
+      leaves |= x != 0;
+    }
+    const uint64_t bmask = __ballot(in && leaves);
+    if (lane == ww) bdw = bmask;
+    if (in) {
+      const int32_t tv = T[v], mv = M[v];
+      tl += tv;
+      ml += mv;
+      if (leaves) {
+        tb += tv;
+        mb += mv;
+      }
+    }
+  }
+  uint64_t out = 0;                                   // word `lane` of delta+(L) \ L
+#pragma unroll
+  for (int w = 0; w < kLaneWords; w++) {
+    if (w >= words) break;
+    const uint64_t r = wave_or_u64(acc[w]);
+    if (lane == w) out = r;
+  }
+  // delta-(delta+(L) \ L) \ L, and M of both sets
+#pragma unroll
+  for (int w = 0; w < kLaneWords; w++) acc[w] = 0;
+  int64_t ao = 0;
+#pragma unroll
+  for (int ww = 0; ww < kLaneWords; ww++) {
+    if (ww >= words) break;
+    const int v = ww * 64 + lane;
+    const bool in = (readlane_u64(out, ww) >> lane) & 1ull;
+    if (!in) continue;
+    ao += M[v];
+#pragma unroll
+    for (int w = 0; w < kLaneWords; w++) {
+      if (w >= words) break;
+      acc[w] |= pred[(int64_t)v * words + w] & ~Lw[w];
+    }
+  }
+  int64_t ai = 0;
+#pragma unroll
+  for (int w = 0; w < kLaneWords; w++) {
+    if (w >= words) break;
+    const uint64_t in2w = wave_or_u64(acc[w]);        // word w, the same on every lane
+    if ((in2w >> lane) & 1ull) ai += M[w * 64 + lane];
+  }
+  tl = wave_sum_i64(tl);
+  ml = wave_sum_i64(ml);
+  tb = wave_sum_i64(tb);
+  mb = wave_sum_i64(mb);
+  ao = wave_sum_i64(ao);
+  ai = wave_sum_i64(ai);
+  const int sz = (int)wave_sum_i64(lane < words ? __popcll(L) : 0);
+  if (lane < words) bd[(int64_t)lane * fstride + s] = bdw;
+  if (lane == 0) {
+    size[s] = sz;
+    Tsum[s] = (int32_t)tl;
+    Msum[s] = (int32_t)ml;
+    Tbd[s] = (int32_t)tb;
+    Mbd[s] = (int32_t)mb;
+    A[s] = (int32_t)(ao + ai);
+    w_out[s] = (int32_t)(tl - tb + 1);
+  }
+}
+
 __global__ void k_row_widths(int64_t F, const int32_t* w, int64_t* padded) {
   const int64_t s = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   if (s < F) padded[s] = ((int64_t)w[s] + kRowAlign - 1) / kRowAlign * kRowAlign;
@@ -556,6 +725,12 @@ hipError_t launch_graph_masks(rc_graph g, const int32_t* d_row_ptr, const int32_
 }
 
 hipError_t launch_ancestors(rc_graph g, uint64_t* anc, hipStream_t s) {
+  const size_t lds_closure = sizeof(uint64_t) * (size_t)g->n * g->words;
+  if (g->words <= kClosureWords && (int64_t)g->n * g->words <= kClosureItems * kClosureThreads) {
+    hipLaunchKernelGGL(k_ancestors_closure, dim3(1), dim3(kClosureThreads), lds_closure, s, g->n,
+                       g->words, g->dPred, anc);
+    return hipGetLastError();
+  }
   const size_t lds_wave = sizeof(uint64_t) * (size_t)g->n * g->words +
                           sizeof(int32_t) * ((size_t)g->n + 1 + g->num_pred_edges + g->n);
   if (lds_wave <= 64 * 1024) {
@@ -613,6 +788,17 @@ hipError_t launch_set_quantities(rc_family f, hipStream_t s) {
   const int per_block = 256 / kWave;
   const dim3 grid((unsigned)((f->F + per_block - 1) / per_block));
   const size_t lds = 2 * sizeof(uint64_t) * (size_t)g->n * g->words;
+  if (g->words <= kLaneWords) {
+    if (lds <= 64 * 1024)
+      hipLaunchKernelGGL(k_set_quantities_lanes<true>, grid, dim3(256), lds, s, f->F, g->n,
+                         g->words, f->fstride, f->bits, g->dSucc, g->dPred, g->dT, g->dM, f->bd,
+                         f->size, f->Tsum, f->Msum, f->Tbd, f->Mbd, f->A, f->w);
+    else
+      hipLaunchKernelGGL(k_set_quantities_lanes<false>, grid, dim3(256), 0, s, f->F, g->n,
+                         g->words, f->fstride, f->bits, g->dSucc, g->dPred, g->dT, g->dM, f->bd,
+                         f->size, f->Tsum, f->Msum, f->Tbd, f->Mbd, f->A, f->w);
+    return hipGetLastError();
+  }
   if (lds <= 64 * 1024)
     hipLaunchKernelGGL(k_set_quantities<true>, grid, dim3(256), lds, s, f->F, g->n, g->words,
                        f->fstride, f->bits, g->dSucc, g->dPred, g->dT, g->dM, f->bd, f->size,
