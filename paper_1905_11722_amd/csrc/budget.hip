@@ -9,11 +9,13 @@
 //                     over the pairs with f[L] + c(L, L') <= B,
 // and B is feasible exactly when f[V] is finite.  Feasibility is monotone
 // in B and B = 2 M(V) is always feasible (the one-segment chain {V} peaks at
-// 2 M(V)), so the search runs over [0, 2 M(V)].  One wave evaluates 64
+// 2 M(V)), so the search runs over [0, 2 M(V)].  Each round evaluates 64
 // budgets at once, one per lane, spread over the open interval between the
 // largest budget known infeasible and the smallest known feasible; each
 // round shrinks that interval 65-fold, so at most three rounds reach a
-// budget range of 2^16.
+// budget range of 2^16.  When f fits LDS, 16 waves share a target's pairs
+// (k_min_budget_waves); otherwise one wave walks them with f in global
+// scratch (k_min_budget).
 #include <hip/hip_runtime.h>
 
 #include "rc_internal.h"
@@ -77,13 +79,101 @@ __global__ __launch_bounds__(kLanes) void k_min_budget(int64_t F, int32_t hi0,
   if (lane == 0) st->bmin = hi;
 }
 
+// The same search with the pairs of a target spread over kMbWaves waves:
+// wave w, lane q holds pair p0 + kMbWaves q + w of the target (one coalesced
+// load per wave, issued a target ahead), every wave relaxes its pairs for
+// the 64 budgets (lane = budget, pair values taken with readlane), and the
+// waves' partial minima meet in LDS.  Two barriers per target instead of a
+// dependent scalar load per pair.
+constexpr int kMbWaves = 16;
+constexpr int kMbChunk = kMbWaves * kLanes;          // pairs per target and pass
+
+template <typename FT>
+__global__ __launch_bounds__(kMbChunk) void k_min_budget_waves(int64_t F, int32_t hi0,
+                                                                const int64_t* pred_ptr,
+                                                                const int32_t* pidx,
+                                                                const int32_t* pdm,
+                                                                const int32_t* pc,
+                                                                DevStatus* st) {
+  constexpr FT kInfF = (FT)~(FT)0;
+  extern __shared__ __attribute__((aligned(16))) unsigned char flds_raw[];
+  FT* f = reinterpret_cast<FT*>(flds_raw);               // [F][64]
+  __shared__ uint32_t red[kMbWaves][kLanes];
+  const int lane = threadIdx.x & (kLanes - 1);
+  const int wave = threadIdx.x / kLanes;
+  cint64* pp = (cint64*)pred_ptr;
+  // pair p0 + kMbWaves * lane + wave of target j (j < F), chunk base p0
+  auto load = [&](int64_t j, int64_t base, int32_t& i, int32_t& dm, int32_t& c) {
+    i = -1;
+    dm = 0;
+    c = 0;
+    if (j >= F) return;
+    const int64_t p = base + (int64_t)kMbWaves * lane + wave;
+    if (p < pp[j + 1]) {
+      i = pidx[p];
+      dm = pdm[p];
+      c = pc[p];
+    }
+  };
+  int32_t lo = -1, hi = hi0;                           // lo infeasible, hi feasible
+  while (hi - lo > 1) {
+    const int64_t span = hi - lo;
+    const int32_t B = lo + (int32_t)(((int64_t)(lane + 1) * span + kLanes) / (kLanes + 1));
+    if (wave == 0) f[lane] = 0;                        // the empty set
+    int32_t ni, ndm, nc;                               // the next target's first chunk
+    load(1, F > 1 ? pp[1] : 0, ni, ndm, nc);
+    __syncthreads();
+    for (int64_t j = 1; j < F; j++) {
+      const int64_t p0 = pp[j], p1 = pp[j + 1];
+      int32_t ci = ni, cdm = ndm, cc = nc;
+      load(j + 1, j + 1 < F ? pp[j + 1] : 0, ni, ndm, nc);
+      uint32_t best = kInfF;
+      for (int64_t base = p0; base < p1; base += kMbChunk) {
+        if (base != p0) load(j, base, ci, cdm, cc);
+        // pairs of this wave in the chunk: base + kMbWaves * q + wave < p1
+        const int64_t rem = p1 - base - wave;
+        const int nq = rem <= 0 ? 0 : (int)min<int64_t>(kLanes, (rem + kMbWaves - 1) / kMbWaves);
+        for (int q = 0; q < nq; q++) {
+          const int32_t i = __builtin_amdgcn_readlane(ci, q);
+          const int32_t dm = __builtin_amdgcn_readlane(cdm, q);
+          const int32_t c = __builtin_amdgcn_readlane(cc, q);
+          const uint32_t fi = f[(int64_t)i * kLanes + lane];
+          if (fi != kInfF && (int64_t)fi + c <= B) {
+            const uint32_t cand = fi + (uint32_t)dm;
+            best = cand < best ? cand : best;
+          }
+        }
+      }
+      red[wave][lane] = best;
+      __syncthreads();
+      if (wave == 0) {
+        uint32_t m = red[0][lane];
+#pragma unroll
+        for (int w = 1; w < kMbWaves; w++) m = min(m, red[w][lane]);
+        f[j * kLanes + lane] = (FT)m;
+      }
+      __syncthreads();
+    }
+    const bool ok = f[(F - 1) * kLanes + lane] != kInfF;
+    const unsigned long long bal = __ballot(ok);
+    const int first = bal ? __ffsll((long long)bal) - 1 : kLanes;
+    const int32_t Bfirst = __shfl(B, first < kLanes ? first : 0, kLanes);
+    const int32_t Bprev = __shfl(B, first > 0 ? first - 1 : 0, kLanes);
+    if (first < kLanes) hi = Bfirst;
+    if (first > 0) lo = first < kLanes ? Bprev : __shfl(B, kLanes - 1, kLanes);
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) st->bmin = hi;
+}
+
 }  // namespace
 
 // Value type and home of f: 16 bits when every finite value (at most
 // 2 M(V)) fits below the infinity code, LDS when [F][64] fits in 64 KB.
 static int min_budget_kind(rc_family f, int32_t hi0) {
-  if (hi0 < 0xFFFF && (size_t)f->F * kLanes * 2 <= 64 * 1024) return 0;
-  if ((size_t)f->F * kLanes * 4 <= 64 * 1024) return 1;
+  // the multi-wave kernel keeps 4 KB of partial minima in LDS beside f
+  if (hi0 < 0xFFFF && (size_t)f->F * kLanes * 2 <= 60 * 1024) return 0;
+  if ((size_t)f->F * kLanes * 4 <= 60 * 1024) return 1;
   return 2;
 }
 
@@ -93,17 +183,20 @@ size_t min_budget_scratch_bytes(rc_family f, int32_t hi0) {
 
 hipError_t launch_min_budget(rc_family f, int32_t hi0, uint32_t* scratch, hipStream_t s) {
   const int kind = min_budget_kind(f, hi0);
-  if (kind == 0)
-    hipLaunchKernelGGL((k_min_budget<uint16_t, true>), dim3(1), dim3(kLanes),
+  if (kind == 0) {
+    hipLaunchKernelGGL((k_min_budget_waves<uint16_t>), dim3(1), dim3(kMbChunk),
                        sizeof(uint16_t) * (size_t)f->F * kLanes, s, f->F, hi0, f->pred_ptr,
-                       f->pidx, f->pdm, f->pc, (uint16_t*)nullptr, f->status);
-  else if (kind == 1)
-    hipLaunchKernelGGL((k_min_budget<uint32_t, true>), dim3(1), dim3(kLanes),
+                       f->pidx, f->pdm, f->pc, f->status);
+    return hipGetLastError();
+  }
+  if (kind == 1) {
+    hipLaunchKernelGGL((k_min_budget_waves<uint32_t>), dim3(1), dim3(kMbChunk),
                        sizeof(uint32_t) * (size_t)f->F * kLanes, s, f->F, hi0, f->pred_ptr,
-                       f->pidx, f->pdm, f->pc, (uint32_t*)nullptr, f->status);
-  else
-    hipLaunchKernelGGL((k_min_budget<uint32_t, false>), dim3(1), dim3(kLanes), 0, s, f->F, hi0,
-                       f->pred_ptr, f->pidx, f->pdm, f->pc, scratch, f->status);
+                       f->pidx, f->pdm, f->pc, f->status);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL((k_min_budget<uint32_t, false>), dim3(1), dim3(kLanes), 0, s, f->F, hi0,
+                     f->pred_ptr, f->pidx, f->pdm, f->pc, scratch, f->status);
   return hipGetLastError();
 }
 

@@ -281,6 +281,21 @@ def test_min_budget_random(rc, oracle_mod, n, p, seed, mode):
     assert fam.min_budget() == oracle_mod.min_budget(g, mode)
 
 
+def test_min_budget_value_widths_and_large_families(rc, oracle_mod):
+    """rc_min_budget where f needs 32 bits (2 M(V) above the 16-bit codes)
+    and where the family's f table does not fit LDS (1024 sets)."""
+    big = W.chain(6, seed=3, tmax=9, mmax=8)
+    big = W.Graph(big.n, big.succ, big.T, [15000 + 997 * v for v in range(big.n)])
+    assert 2 * sum(big.M) > 0xFFFF
+    for mode in ("exact", "pruned"):
+        fam = rc.Graph.create(big).build_family(mode)
+        assert fam.min_budget() == oracle_mod.min_budget(big, mode)
+    wide = W.antichain(10, seed=5, tmax=3, mmax=6)
+    fam = rc.Graph.create(wide).build_family("exact")
+    assert fam.info["num_sets"] == 1024
+    assert fam.min_budget() == oracle_mod.min_budget(wide, "exact")
+
+
 @pytest.mark.parametrize("name", ["chain16", "layered24", "ladder40", "unet", "resnet50",
                                   "densenet121"])
 def test_min_budget_workloads(rc, name):
