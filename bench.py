@@ -34,8 +34,10 @@ if ROOT not in sys.path:
 VALU_INT32_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
 VALU_U16_PEAK_TOPS = 2 * VALU_INT32_PEAK_TOPS
 OPS_PER_RELAXATION = 3          # compare with tau, add dm, min into the target
-FILL_SOURCES = ["paper_1905_11722_amd/csrc/fill.hip", "paper_1905_11722_amd/csrc/blocked.hip",
-                "paper_1905_11722_amd/csrc/blocks.hip", "paper_1905_11722_amd/csrc/wavefront.h"]
+# The sources that shape the row-push fill kernel and its traffic: the
+# kernel, its record preparation, the shared helpers and constants.
+FILL_SOURCES = ["paper_1905_11722_amd/csrc/blocked.hip", "paper_1905_11722_amd/csrc/blocks.hip",
+                "paper_1905_11722_amd/csrc/wavefront.h", "paper_1905_11722_amd/csrc/rc_internal.h"]
 
 
 def fill_source_hash():

@@ -165,6 +165,7 @@ __global__ void k_select_finish(const uint16_t* m, const int64_t* row_off, int64
 constexpr int kTraceThreads = 512;
 constexpr int kTraceLds = 2048;       // families up to this size keep their per-set arrays in LDS
 
+template <bool kLds>
 __global__ __launch_bounds__(kTraceThreads) void k_trace(
     int64_t F, int n, int words, int64_t fstride, const uint64_t* __restrict__ bits,
     const uint64_t* __restrict__ bd, const int32_t* __restrict__ A, const int32_t* __restrict__ T,
@@ -187,8 +188,7 @@ __global__ __launch_bounds__(kTraceThreads) void k_trace(
   __shared__ int32_t s_M[kMaxNodes];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1), wave = tid / kWave;
-  const bool in_lds = F <= kTraceLds;
-  if (in_lds) {
+  if (kLds) {
     for (int64_t x = tid; x < F; x += kTraceThreads) {
       s_w[x] = w[x];
       s_off[x] = row_off[x];
@@ -207,9 +207,9 @@ __global__ __launch_bounds__(kTraceThreads) void k_trace(
     if (acc == 0x7fffffff) st->pad0 = acc;          // keeps the loads
   }
   __syncthreads();
-  auto Wd = [&](int64_t i) { return in_lds ? s_w[i] : w[i]; };
-  auto Off = [&](int64_t i) { return in_lds ? s_off[i] : row_off[i]; };
-  auto PP = [&](int64_t i) { return in_lds ? s_pp[i] : pred_ptr[i]; };
+  auto Wd = [&](int64_t i) { return kLds ? s_w[i] : w[i]; };
+  auto Off = [&](int64_t i) { return kLds ? s_off[i] : row_off[i]; };
+  auto PP = [&](int64_t i) { return kLds ? s_pp[i] : pred_ptr[i]; };
 
   // The walk is identical in every thread; only the predecessor scan is split.
   int64_t j = F - 1;
@@ -222,23 +222,22 @@ __global__ __launch_bounds__(kTraceThreads) void k_trace(
       bad = true;
       break;
     }
-    const uint32_t mj = m[Off(j) + t];
     const int64_t p0 = PP(j), p1 = PP(j + 1);
+    const uint32_t mj = m[Off(j) + t];
     int32_t next_i = -1, next_dt = 0;
     for (int64_t base = p0; base < p1 && next_i < 0; base += kTraceThreads) {
+      // every load of a chunk is issued unconditionally (a thread past the
+      // list reads the list's first pair, a source cell out of its row reads
+      // the row's first cell) and the tests come last, so a step waits for
+      // the pair data, the source rows' extents and the source cells only
       const int64_t p = base + tid;
-      bool hit = false;
-      int32_t i = 0, dt = 0;
-      if (p < p1) {
-        i = pidx[p];
-        dt = pdt[p];
-        const int32_t c = pc[p], dm = pdm[p];
-        const int64_t ts = t - dt;
-        if (ts >= 0 && ts < Wd(i)) {
-          const int32_t x = m[Off(i) + ts];
-          hit = x <= Beff - c && (uint32_t)(x + dm) == mj;
-        }
-      }
+      const bool valid = p < p1;
+      const int64_t pq = valid ? p : p0;
+      const int32_t i = pidx[pq], dt = pdt[pq], c = pc[pq], dm = pdm[pq];
+      const int64_t ts = t - dt;
+      const bool inrow = valid && ts >= 0 && ts < Wd(i);
+      const int32_t x = m[Off(i) + (inrow ? ts : 0)];
+      const bool hit = inrow && x <= Beff - c && (uint32_t)(x + dm) == mj;
       const unsigned long long bal = __ballot(hit);
       if (lane == 0) s_first[par][wave] = bal ? wave * kWave + __ffsll((long long)bal) - 1 : INT32_MAX;
       s_src[par][tid] = i;
@@ -363,10 +362,16 @@ hipError_t launch_select(rc_solution sol, hipStream_t s) {
 hipError_t launch_trace(rc_solution sol, hipStream_t s) {
   rc_family f = sol->f;
   rc_graph g = f->g;
-  hipLaunchKernelGGL(k_trace, dim3(1), dim3(kTraceThreads), 0, s, f->F, g->n, g->words,
-                     f->fstride, f->bits, f->bd, f->A, g->dT, g->dM, f->w, f->row_off,
-                     f->pred_ptr, f->pidx, f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, sol->m,
-                     g->T_total, sol->status, sol->chain, sol->seg, sol->cached);
+  if (f->F <= kTraceLds)
+    hipLaunchKernelGGL(k_trace<true>, dim3(1), dim3(kTraceThreads), 0, s, f->F, g->n, g->words,
+                       f->fstride, f->bits, f->bd, f->A, g->dT, g->dM, f->w, f->row_off,
+                       f->pred_ptr, f->pidx, f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, sol->m,
+                       g->T_total, sol->status, sol->chain, sol->seg, sol->cached);
+  else
+    hipLaunchKernelGGL(k_trace<false>, dim3(1), dim3(kTraceThreads), 0, s, f->F, g->n, g->words,
+                       f->fstride, f->bits, f->bd, f->A, g->dT, g->dM, f->w, f->row_off,
+                       f->pred_ptr, f->pidx, f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, sol->m,
+                       g->T_total, sol->status, sol->chain, sol->seg, sol->cached);
   return hipGetLastError();
 }
 
