@@ -53,6 +53,7 @@
 #include <cstdio>
 #include <cstdlib>
 
+#include "ghost_cut.h"
 #include "rc_internal.h"
 #include "wavefront.h"
 
@@ -499,44 +500,7 @@ hipError_t launch_kernel(const GParams& prm, const GParams* gps, int32_t nb, int
 }  // namespace
 
 std::vector<int32_t> ghost_cut(int64_t F, const std::vector<int32_t>& near) {
-  std::vector<int32_t> bstart;
-  if (F < 2) {
-    bstart.push_back(1);
-    return bstart;
-  }
-  // e(r, r2) of rows r < r2 of the open block, from the near shifts of r2
-  auto shift = [&](int64_t r, int64_t r2) -> int32_t {
-    const int64_t d = r2 - r;
-    return d >= 1 && d <= kNear ? near[r2 * kNear + d - 1] : -1;
-  };
-  int64_t start = 1;
-  bstart.push_back(1);
-  for (int64_t j = 2; j < F; j++) {
-    // would rows start .. j still fit?  cone(j) = 0, then backwards
-    bool fits = j - start < kJB;
-    int32_t cone[kJB];
-    const int64_t len = j - start + 1;
-    for (int64_t r = len - 1; fits && r >= 0; r--) {
-      int32_t cr = 0;
-      for (int64_t r2 = r + 1; r2 < len; r2++) {
-        const int32_t e = shift(start + r, start + r2);
-        if (e < 0) continue;
-        if (e > kGhostHalo) {
-          fits = false;
-          break;
-        }
-        cr = std::max(cr, cone[r2] + e);
-      }
-      cone[r] = cr;
-      if (cr > kGhostHalo) fits = false;
-    }
-    if (!fits) {
-      start = j;
-      bstart.push_back((int32_t)j);
-    }
-  }
-  bstart.push_back((int32_t)F);
-  return bstart;
+  return ghost_cut_rows(F, near, kNear, kJB, kGhostHalo);
 }
 
 hipError_t launch_near_shifts(rc_family f, int32_t* near, hipStream_t s) {
