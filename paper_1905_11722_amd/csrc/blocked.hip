@@ -205,21 +205,13 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p0, const BPa
         const int kk = 2 * wave + h;
         bool valid;
         (void)rec_of(k, kk, valid);
-        const int32_t* hd = s_hdr[k % NH][kk];
-        const int32_t emin = hd[1], span = hd[2], Pi = hd[3];
-        const int64_t endi = (int64_t)(uint32_t)hd[4] | ((int64_t)hd[5] << 32);
-        const int32_t us = u0 + emin;
-        const bool live_rec = valid && us <= 0 && us + C - 1 + span >= -Pi;
-        const int64_t astart = endi + us - (emin & 7);
-        const int64_t E = endi + 1;
-        const int64_t S = E - (int64_t)((Pi + kRowAlign) / kRowAlign) * kRowAlign;
+        const WinDma wd = win_dma(s_hdr[k % NH][kk], valid, u0, C, p.m);
 #pragma unroll
         for (int i = 0; i < IPR; i++) {
           const int32_t kc = lane + 64 * i;
           if (kc < NCH) {
-            const int64_t cell = astart + 8 * (int64_t)kc;
-            const bool ok = live_rec && cell >= S && cell + 8 <= E;
-            dma16(ok ? (const void*)(p.m + cell) : (const void*)p.sentinel,
+            const bool ok = kc >= wd.lo && kc < wd.hi;
+            dma16(ok ? (const void*)(wd.base + 8 * kc) : (const void*)p.sentinel,
                   __builtin_amdgcn_readfirstlane(lds_addr(&s_win[k % NW][kk][512 * i])));
           }
         }

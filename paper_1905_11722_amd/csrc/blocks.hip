@@ -196,7 +196,10 @@ __global__ __launch_bounds__(256) void k_blk_clusters(const int64_t* rec_ptr, Bl
 // window starts on a 16-byte boundary, a cells before the cell of shift
 // emin), [8 + s] a + shift - emin of slot s (its cell in the window),
 // [16 + p] budgets B - c of slots 2p, 2p+1 as two uint16, [20 + p] the
-// additions dm of slots 2p, 2p+1 as two uint16.  A slot without a live pair
+// additions dm of slots 2p, 2p+1 as two uint16, [24 .. 29] the window DMA
+// terms that do not depend on the column: [24 .. 25] base = the cell u = 0
+// of row i + emin - a (int64), [26] the cells of row i's 64-aligned slot,
+// [27] emin - a, [28] emin, [29] emax + P_i.  A slot without a live pair
 // gets budget 0 and addition 0xFFFF, so its candidate always saturates to
 // infinity.  meta[b * kMetaInts] = {records, largest live shift, rows of
 // the block, largest P of its rows, (set by k_rec_sort), largest live
@@ -279,7 +282,14 @@ __global__ __launch_bounds__(256) void k_rec_prepare(const int32_t* bstart, int3
         d[16 + x] = (int32_t)tau2[x];
         d[20 + x] = (int32_t)dm2[x];
       }
-      for (int x = 24; x < kRecInts; x++) d[x] = 0;
+      const int64_t base_cell = endi + emin - (emin & 7);
+      d[kRecDma + 0] = (int32_t)(base_cell & 0xFFFFFFFF);
+      d[kRecDma + 1] = (int32_t)(base_cell >> 32);
+      d[kRecDma + 2] = (int32_t)((Pi + kRowAlign) / kRowAlign * kRowAlign);
+      d[kRecDma + 3] = emin - (emin & 7);
+      d[kRecDma + 4] = emin;
+      d[kRecDma + 5] = emax + Pi;
+      for (int x = kRecDma + 6; x < kRecInts; x++) d[x] = 0;
       atomicMax(ghost && i >= prev ? &s_emax_new : &s_emax, emax);
       o++;
     }

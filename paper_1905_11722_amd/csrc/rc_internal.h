@@ -21,6 +21,8 @@ constexpr int64_t kRowAlign = 64;               // cells; rows start on 128-byte
 constexpr int kJB = 8;                          // blocked fill: targets per block
 constexpr int64_t kMaxRecords = (int64_t)1 << 21;  // blocked fill: cap on panel records
 constexpr int kRecInts = 32;                    // blocked fill: int32 per compact record
+constexpr int kRecDma = 24;                     // blocked fill: first record word of the
+                                                // column-independent window DMA terms
 constexpr int kSpan = 248;                      // blocked fill: shifts staged together
 constexpr int kHalo = 512;                      // blocked fill: row pushes with shift <= kHalo
                                                 // read the row's halo, larger ones a window

@@ -72,6 +72,37 @@ __device__ __forceinline__ int32_t ld_relaxed(const gint32* p) {
 
 __device__ __forceinline__ u16x2 as_u16x2(int32_t v) { return __builtin_bit_cast(u16x2, v); }
 
+// The window DMA of one staged record for the column whose first computed
+// cell lies at distance u0 from the row end and that computes cw cells: the
+// window starts at table cell base + u0 and its 16-byte chunk kc is loaded
+// when lo <= kc < hi (inside the source row's aligned slot, and the record
+// reaches the column), else the infinity sentinel is.  The terms that do
+// not depend on the column come precomputed with the record (words kRecDma
+// ..), so a record costs a few scalar operations and two compares per lane.
+struct WinDma {
+  const uint16_t* base;
+  int32_t lo, hi;
+};
+
+__device__ __forceinline__ WinDma win_dma(const int32_t* hd, bool valid, int32_t u0, int32_t cw,
+                                          const uint16_t* m) {
+  const int4 h = *reinterpret_cast<const int4*>(hd + kRecDma);
+  const int2 g = *reinterpret_cast<const int2*>(hd + kRecDma + 4);
+  const uint32_t blo = __builtin_amdgcn_readfirstlane(h.x);
+  const int32_t bhi = __builtin_amdgcn_readfirstlane(h.y);
+  const int32_t span = __builtin_amdgcn_readfirstlane(h.z);    // cells of the row's slot
+  const int32_t er = __builtin_amdgcn_readfirstlane(h.w);      // emin - a
+  const int32_t emin = __builtin_amdgcn_readfirstlane(g.x);
+  const int32_t far = __builtin_amdgcn_readfirstlane(g.y);     // emax + P_i
+  const bool live = valid && u0 + emin <= 0 && u0 + cw - 1 + far >= 0;
+  const int32_t to_end = 1 - u0 - er;                          // cells from the window start to the row end
+  WinDma w;
+  w.base = m + ((((int64_t)bhi << 32) | blo) + u0);
+  w.hi = live ? to_end >> 3 : 0;
+  w.lo = (to_end - span) >> 3;
+  return w;
+}
+
 // Two relaxations of Algorithm 1: m' = x + dm if x <= tau (tau = B - c, the
 // budget test), else infinity, in packed unsigned 16-bit lanes with
 // saturation.  y = x +sat dm; q = x -sat tau is nonzero exactly when the
