@@ -84,6 +84,7 @@ struct Geo {
   static constexpr int CPL = C / kWave;            // cells per control lane when storing a row
   static_assert(kSpan + 7 <= 256, "panel window");
   static_assert(NI * (D - 1) < 63, "vmcnt range");
+  static_assert(D < NW && 2 * D < NH, "buffer counters wrap at most once");
 };
 
 
@@ -177,6 +178,7 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p0, const BPa
     // (grant > pb), requests the first headers, then their windows, then
     // computes one stage per step.
     int32_t pb = -1, pn = 0, pns = 0, pSU = 0, pnU = 0, pnG = 0, pnu = 0, pphase = 0;
+    int32_t pw = 0, ph = 0;                        // pn % NW and pn % NH, kept as counters
     const int32_t* pcrec = p.crec;
     int32_t poll_reach = 0, poll_need = 0;         // control: what the grant waits for
     long long poll_t0 = 0;
@@ -191,28 +193,29 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p0, const BPa
       valid = r < pnG;
       return valid ? pnu + r : 0;
     };
-    auto issue_hdr = [&](int32_t k) __attribute__((always_inline)) {   // compute waves
+    // stage k goes to window buffer wb = k % NW and header buffer hb = k % NH
+    auto issue_hdr = [&](int32_t k, int hb) __attribute__((always_inline)) {   // compute waves
       if (lane < 16) {
         bool valid;
         const int32_t r = rec_of(k, 2 * wave + (lane >> 3), valid);
         const int32_t* src = pcrec + (int64_t)r * kRecInts + (lane & 7) * 4;
-        dma16(src, __builtin_amdgcn_readfirstlane(lds_addr(&s_hdr[k % NH][2 * wave][0])));
+        dma16(src, __builtin_amdgcn_readfirstlane(lds_addr(&s_hdr[hb][2 * wave][0])));
       }
     };
-    auto issue_win = [&](int32_t k) __attribute__((always_inline)) {   // compute waves
+    auto issue_win = [&](int32_t k, int wb, int hb) __attribute__((always_inline)) {
 #pragma unroll
       for (int h = 0; h < 2; h++) {
         const int kk = 2 * wave + h;
         bool valid;
         (void)rec_of(k, kk, valid);
-        const WinDma wd = win_dma(s_hdr[k % NH][kk], valid, u0, C, p.m);
+        const WinDma wd = win_dma(s_hdr[hb][kk], valid, u0, C, p.m);
 #pragma unroll
         for (int i = 0; i < IPR; i++) {
           const int32_t kc = lane + 64 * i;
           if (kc < NCH) {
             const bool ok = kc >= wd.lo && kc < wd.hi;
             dma16(ok ? (const void*)(wd.base + 8 * kc) : (const void*)p.sentinel,
-                  __builtin_amdgcn_readfirstlane(lds_addr(&s_win[k % NW][kk][512 * i])));
+                  __builtin_amdgcn_readfirstlane(lds_addr(&s_win[wb][kk][512 * i])));
           }
         }
       }
@@ -221,8 +224,7 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p0, const BPa
     // per record: a record past the list or whose window misses the source
     // row was staged from the infinity sentinel, so its candidates are
     // infinite.
-    auto compute = [&](int32_t k) __attribute__((always_inline)) {
-      const int wb = k % NW, hb = k % NH;
+    auto compute = [&](int32_t k, int wb, int hb) __attribute__((always_inline)) {
       if (k < pSU) {                     // every slot of these records has one shift
 #pragma unroll
         for (int kk = 0; kk < kNB; kk++) {
@@ -266,6 +268,8 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p0, const BPa
     auto pipe_setup = [&](int32_t b1, int32_t need) __attribute__((always_inline)) {
       pb = b1;
       pn = 0;
+      pw = 0;
+      ph = 0;
       pns = 0;
       pphase = 0;
       if (b1 >= p.nblk) return;
@@ -286,6 +290,8 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p0, const BPa
     // the pipeline state is the same in every lane: keep it in scalars
     auto uniform = [&]() __attribute__((always_inline)) {
       pn = __builtin_amdgcn_readfirstlane(pn);
+      pw = __builtin_amdgcn_readfirstlane(pw);
+      ph = __builtin_amdgcn_readfirstlane(ph);
       pns = __builtin_amdgcn_readfirstlane(pns);
       pphase = __builtin_amdgcn_readfirstlane(pphase);
       pSU = __builtin_amdgcn_readfirstlane(pSU);
@@ -312,23 +318,28 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p0, const BPa
       if (pn < pns) {
         if (pphase == 2) {
           if (!ctl) {
-            compute(pn);
+            compute(pn, pw, ph);
             if (pn + D < pns) {
-              issue_win(pn + D);
-              issue_hdr(pn + 2 * D);
+              const int pwD = pw + D >= NW ? pw + D - NW : pw + D;
+              const int phD = ph + D >= NH ? ph + D - NH : ph + D;
+              const int ph2D = ph + 2 * D >= NH ? ph + 2 * D - NH : ph + 2 * D;
+              issue_win(pn + D, pwD, phD);
+              issue_hdr(pn + 2 * D, ph2D);
             }
           }
           ++pn;
+          pw = pw + 1 == NW ? 0 : pw + 1;
+          ph = ph + 1 == NH ? 0 : ph + 1;
         } else if (pphase == 1) {
           if (!ctl)
             for (int32_t k = 0; k < D; k++) {
-              issue_win(k);
-              issue_hdr(k + D);
+              issue_win(k, k % NW, k % NH);
+              issue_hdr(k + D, (k + D) % NH);
             }
           pphase = 2;
         } else if (grant > pb) {
           if (!ctl)
-            for (int32_t k = 0; k < D; k++) issue_hdr(k);
+            for (int32_t k = 0; k < D; k++) issue_hdr(k, k % NH);
           pphase = 1;
         }
       }
