@@ -83,6 +83,7 @@ struct GGeo {
   static_assert(C % 64 == 0, "a column holds whole 128-byte lines");
   static_assert(WIN % 8 == 0 && kSpan + 8 <= 256, "panel window");
   static_assert(NI * (D - 1) < 63, "vmcnt range");
+  static_assert(D < NWB && 2 * D < NHB, "buffer counters wrap at most once");
 };
 
 template <int CPT>
@@ -181,29 +182,30 @@ __global__ __launch_bounds__(kGT) void k_fill_ghost(GParams p0, const GParams* g
         valid = r < nN;
         return valid ? nOall + r : 0;
       };
-      auto issue_hdr = [&](int32_t k) __attribute__((always_inline)) {
+      // stage k goes to window buffer wb = k % NWB and header buffer hb = k % NHB
+      auto issue_hdr = [&](int32_t k, int hb) __attribute__((always_inline)) {
         if (dmaw && lane < 16) {
           bool valid;
           const int32_t r = rec_of(k, 2 * wave + (lane >> 3), valid);
           const int32_t* src = pcrec + (int64_t)r * kRecInts + (lane & 7) * 4;
-          dma16(src, __builtin_amdgcn_readfirstlane(lds_addr(&s_hdr[k % NHB][2 * wave][0])));
+          dma16(src, __builtin_amdgcn_readfirstlane(lds_addr(&s_hdr[hb][2 * wave][0])));
         }
       };
-      auto issue_win = [&](int32_t k) __attribute__((always_inline)) {
+      auto issue_win = [&](int32_t k, int wb, int hb) __attribute__((always_inline)) {
         if (!dmaw) return;
 #pragma unroll
         for (int h = 0; h < 2; h++) {
           const int kk = 2 * wave + h;
           bool valid;
           (void)rec_of(k, kk, valid);
-          const WinDma wd = win_dma(s_hdr[k % NHB][kk], valid, u0, CH, p.m);
+          const WinDma wd = win_dma(s_hdr[hb][kk], valid, u0, CH, p.m);
 #pragma unroll
           for (int i = 0; i < IPR; i++) {
             const int32_t kc = lane + 64 * i;
             if (kc < NCH) {
               const bool ok = kc >= wd.lo && kc < wd.hi;
               dma16(ok ? (const void*)(wd.base + 8 * kc) : (const void*)p.sentinel,
-                    __builtin_amdgcn_readfirstlane(lds_addr(&s_win[k % NWB][kk][512 * i])));
+                    __builtin_amdgcn_readfirstlane(lds_addr(&s_win[wb][kk][512 * i])));
             }
           }
         }
@@ -227,8 +229,7 @@ __global__ __launch_bounds__(kGT) void k_fill_ghost(GParams p0, const GParams* g
           for (int q = 0; q < CPT; q++) acc[x][q] = kInf2;
 
         // ---------------- panel
-        auto compute = [&](int32_t k) __attribute__((always_inline)) {
-          const int wb = k % NWB, hb = k % NHB;
+        auto compute = [&](int wb, int hb) __attribute__((always_inline)) {
 #pragma unroll
           for (int kk = 0; kk < kNB; kk++) {
             const int4* h4 = reinterpret_cast<const int4*>(s_hdr[hb][kk]);
@@ -250,15 +251,16 @@ __global__ __launch_bounds__(kGT) void k_fill_ghost(GParams p0, const GParams* g
         };
         if (S > 0) {
 #pragma unroll
-          for (int32_t k = 0; k < D; k++) issue_hdr(k);
+          for (int32_t k = 0; k < D; k++) issue_hdr(k, k % NHB);
           wait_vm<0>();
           bar();
           if (!gate_for(S < D ? S - 1 : D - 1)) return false;
 #pragma unroll
           for (int32_t k = 0; k < D; k++) {
-            issue_win(k);
-            issue_hdr(k + D);
+            issue_win(k, k % NWB, k % NHB);
+            issue_hdr(k + D, (k + D) % NHB);
           }
+          int wb = 0, hb = 0;                          // k % NWB, k % NHB
           for (int32_t k = 0; k < S; k++) {
             if (dmaw) {
               if (k + D <= S)
@@ -267,12 +269,15 @@ __global__ __launch_bounds__(kGT) void k_fill_ghost(GParams p0, const GParams* g
                 wait_vm<0>();
             }
             bar();
-            compute(k);
+            compute(wb, hb);
             if (k + D < S) {
               if (!gate_for(k + D)) return false;
-              issue_win(k + D);
-              issue_hdr(k + 2 * D);
+              issue_win(k + D, wb + D >= NWB ? wb + D - NWB : wb + D,
+                        hb + D >= NHB ? hb + D - NHB : hb + D);
+              issue_hdr(k + 2 * D, hb + 2 * D >= NHB ? hb + 2 * D - NHB : hb + 2 * D);
             }
+            wb = wb + 1 == NWB ? 0 : wb + 1;
+            hb = hb + 1 == NHB ? 0 : hb + 1;
           }
         }
 
