@@ -134,17 +134,25 @@ __global__ __launch_bounds__(kFillThreads) void k_arg_all(
 }
 
 // t* = min (time-centric) or max (memory-centric) finite t of row V.
+// Each wave reduces its cells' candidate first and issues one atomic, so
+// that a row of mostly finite cells does not serialize on one address.
 __global__ void k_select(const uint16_t* m, const int64_t* row_off, int64_t v, const int32_t* w,
                          int objective, DevStatus* st) {
   const int64_t off = row_off[v];
   const int32_t wv = w[v];
-  for (int32_t t = blockIdx.x * blockDim.x + threadIdx.x; t < wv; t += gridDim.x * blockDim.x) {
-    if (m[off + t] != kInfM) {
-      if (objective == RC_TIME_CENTRIC)
-        atomicMin(&st->t_sel, t);
-      else
-        atomicMax(&st->t_sel, t);
-    }
+  const bool tc = objective == RC_TIME_CENTRIC;
+  int32_t best = tc ? INT32_MAX : -1;
+  for (int32_t t = blockIdx.x * blockDim.x + threadIdx.x; t < wv; t += gridDim.x * blockDim.x)
+    if (m[off + t] != kInfM) best = tc ? min(best, t) : max(best, t);
+  for (int o = kWave / 2; o > 0; o >>= 1) {
+    const int32_t y = __shfl_xor(best, o, kWave);
+    best = tc ? min(best, y) : max(best, y);
+  }
+  if ((threadIdx.x & (kWave - 1)) == 0 && (tc ? best != INT32_MAX : best >= 0)) {
+    if (tc)
+      atomicMin(&st->t_sel, best);
+    else
+      atomicMax(&st->t_sel, best);
   }
 }
 
