@@ -1,0 +1,183 @@
+"""Memory-indexed form of Algorithm 1's recursion -- test infrastructure.
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg may use
+this module.  It shares nothing with the GPU library and nothing with the C
+oracle: the family, the per-set and per-pair quantities are formed here from
+their definitions in Sections 2-4 with numpy boolean arrays over node ids.
+
+Algorithm 1 (Section 4.2, Appendix A) walks states (L, t, m): a chain that
+ends at lower set L with forward time t and cached memory m = M(U).  A
+transition L -> L' (L a proper subset of L') is allowed when m + c <= B,
+c = 2 M(L' \\ L) + M(delta+(L') \\ L') + M(delta-(delta+(L')) \\ L') (Eq. 2),
+and leads to (L', t + T((L' \\ L) \\ boundary(L')), m + M(boundary(L') \\ L)).
+Algorithm 1 keeps, per (L, t), the least m; the budget test is monotone in
+m, so nothing reachable in t is lost.  The same reachable set can be kept per
+(L, m) instead: the least t for the time-centric objective (a later step adds
+the same time to either state, so the faster one is never worse), the
+greatest t for the memory-centric one (Section 4.4).  Then
+
+    t*  = min over m of  tmin[V, m],   t_MC = max over m of tmax[V, m],
+
+and opt[V, t*] of Algorithm 1 is the least m with tmin[V, m] = t* (resp.
+tmax[V, m] = t_MC).  Rows run over m in [0, min(B, M(V))]: every cached
+memory is a sum of distinct node memories (m = M(U), U a subset of V).
+
+Pinned by tests/test_oracle_dual.py against Algorithm 1 (the C oracle) and
+against brute force over every chain (tests/bruteforce.py).
+"""
+
+import numpy as np
+
+INF = np.iinfo(np.int64).max // 4
+
+
+def _adjacency(g):
+    n = g.n
+    succ = np.zeros((n, n), dtype=bool)
+    for v in range(n):
+        for w in g.succ[v]:
+            succ[v, w] = True
+    return succ
+
+
+def _topo(succ):
+    """Kahn's order of the DAG."""
+    n = succ.shape[0]
+    indeg = succ.sum(axis=0).astype(int)
+    order = [v for v in range(n) if indeg[v] == 0]
+    k = 0
+    while k < len(order):
+        v = order[k]
+        k += 1
+        for w in np.flatnonzero(succ[v]):
+            indeg[w] -= 1
+            if indeg[w] == 0:
+                order.append(int(w))
+    if len(order) != n:
+        raise ValueError("the graph has a cycle")
+    return order
+
+
+def _ancestors(succ, order):
+    """anc[v]: v and every node with a path to v (Section 4.3's L^v)."""
+    n = succ.shape[0]
+    anc = np.eye(n, dtype=bool)
+    for v in order:                      # predecessors first
+        for p in np.flatnonzero(succ[:, v]):
+            anc[v] |= anc[p]
+    return anc
+
+
+def _lower_sets(succ, order):
+    """Every set closed under predecessors, by deciding the nodes in
+    topological order (a node may join only after all its predecessors)."""
+    n = succ.shape[0]
+    preds = [np.flatnonzero(succ[:, v]) for v in range(n)]
+    out = []
+    cur = np.zeros(n, dtype=bool)
+
+    def rec(k):
+        if k == n:
+            out.append(cur.copy())
+            return
+        v = order[k]
+        rec(k + 1)                       # v left out
+        if all(cur[p] for p in preds[v]):
+            cur[v] = True
+            rec(k + 1)
+            cur[v] = False
+
+    rec(0)
+    return out
+
+
+def family(g, mode):
+    """The family as a bool array [F, n], in ascending size (ties in any
+    order: the optimum does not depend on it).  mode "pruned": the ancestor
+    closures plus the empty set and V (Section 4.3); "exact": every lower
+    set (Section 4.2), by enumeration, for small graphs only."""
+    n = g.n
+    succ = _adjacency(g)
+    order = _topo(succ)
+    if mode == "pruned":
+        sets = [np.zeros(n, bool)] + list(_ancestors(succ, order)) + [np.ones(n, bool)]
+    elif mode == "exact":
+        if n > 40:
+            raise ValueError("exact family enumeration is for small graphs")
+        sets = _lower_sets(succ, order)
+    else:
+        raise ValueError(mode)
+    seen, out = set(), []
+    for L in sets:
+        key = L.tobytes()
+        if key not in seen:
+            seen.add(key)
+            out.append(L)
+    out.sort(key=lambda L: int(L.sum()))
+    return np.array(out, dtype=bool).reshape(len(out), n), succ
+
+
+def solve(g, mode, B, objective="tc"):
+    """(t, m) of the objective, or None when no chain reaches V within B.
+
+    Returns a dict with t, m, the family size, the number of pairs and the
+    relaxations done (one per (pair, m) with m inside the budget window)."""
+    if B < 0:
+        raise ValueError("B < 0")
+    S, succ = family(g, mode)
+    F, n = S.shape
+    T = np.asarray(g.T, dtype=np.int64)
+    M = np.asarray(g.M, dtype=np.int64)
+    width = int(min(B, M.sum())) + 1
+    pred = succ.T
+
+    bd = np.array([L & (succ[:, ~L].any(axis=1)) for L in S])          # boundary(L)
+    out = np.zeros(F, dtype=np.int64)
+    for j in range(F):
+        L = S[j]
+        dp = succ[L].any(axis=0)                                       # delta+(L)
+        dmdp = pred[dp].any(axis=0) if dp.any() else np.zeros(n, bool)  # delta-(delta+(L))
+        out[j] = M[dp & ~L].sum() + M[dmdp & ~L].sum()
+
+    tc = objective == "tc"
+    unreached = INF if tc else -1
+    D = np.full((F, width), unreached, dtype=np.int64)
+    D[0, 0] = 0                                                       # (empty set, t = 0, m = 0)
+    pairs = 0
+    relax = 0
+    for i in range(F):                   # sources in ascending size: every proper subset first
+        L = S[i]
+        for j in range(F):
+            Lp = S[j]
+            if not (Lp & ~L).any() or (L & ~Lp).any():
+                continue                 # L must be a proper subset of L'
+            pairs += 1
+            Vp = Lp & ~L
+            c = 2 * M[Vp].sum() + out[j]
+            dT = T[Vp & ~bd[j]].sum()
+            dM = M[bd[j] & ~L].sum()
+            # source m with m + c <= B; also m + dM <= M(V), which every
+            # reachable m meets (m = M(U) with U inside L, disjoint from the
+            # added boundary), so the clip drops no reachable state
+            top = min(B - c, width - 1 - dM)
+            if top < 0:
+                continue
+            src = D[i, :top + 1]
+            dst = D[j, dM:dM + top + 1]
+            relax += top + 1
+            if tc:
+                cand = np.where(src < INF, src + dT, INF)
+                np.minimum(dst, cand, out=dst)
+            else:
+                cand = np.where(src >= 0, src + dT, -1)
+                np.maximum(dst, cand, out=dst)
+    row = D[F - 1]
+    reach = row < INF if tc else row >= 0
+    result = {"sets": F, "pairs": pairs, "relaxations": relax, "width": width}
+    if not reach.any():
+        result.update(t=None, m=None)
+        return result
+    t = int(row[reach].min()) if tc else int(row[reach].max())
+    m = int(np.flatnonzero(row == t)[0])
+    result.update(t=t, m=m)
+    return result
