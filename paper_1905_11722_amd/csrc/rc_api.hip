@@ -508,6 +508,52 @@ int rc_min_budget(rc_family f, void* stream, int64_t* B_min) {
   return RC_OK;
 }
 
+int rc_solve_dual(rc_family f, int64_t B, int32_t objective, void* stream, int64_t* t_opt,
+                  int64_t* m_opt, float* fill_ms) {
+  if (!f || B < 0) return RC_E_ARG;
+  if (objective != RC_TIME_CENTRIC && objective != RC_MEMORY_CENTRIC) return RC_E_ARG;
+  const int64_t Beff = std::min<int64_t>(B, 2 * f->g->M_total);
+  const int64_t W = std::min<int64_t>(Beff, f->g->M_total) + 1;
+  if (f->g->T_total >= (int64_t)UINT32_MAX || W > INT32_MAX / 2 ||
+      (double)f->F * (double)W > (double)((int64_t)1 << 31))
+    return RC_E_OVERFLOW;
+  hipStream_t s = as_stream(stream);
+  rcdp::Arena A;
+  A.alloc = f->arena.alloc;
+  A.free_fn = f->arena.free_fn;
+  A.user = f->arena.user;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  auto finish = [&](int st) {
+    (void)hipStreamSynchronize(s);
+    if (e0) (void)hipEventDestroy(e0);
+    if (e1) (void)hipEventDestroy(e1);
+    A.release_all();
+    return st;
+  };
+  uint32_t* D = A.get_n<uint32_t>(f->F * W);
+  DevStatus* dst = A.get_n<DevStatus>(1);
+  if (!D || !dst) return finish(RC_E_NOMEM);
+  if (fill_ms && (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess))
+    return finish(RC_E_DEVICE);
+  const hipError_t le = launch_dual(f, (int32_t)Beff, (int32_t)W, objective, D, dst, e0, e1, s);
+  if (le != hipSuccess) {
+    set_last_error("dual table launch", le);
+    return finish(RC_E_DEVICE);
+  }
+  DevStatus hs;
+  if (hipMemcpyAsync(&hs, dst, sizeof(hs), hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return finish(RC_E_DEVICE);
+  if (fill_ms) {
+    float ms = -1.f;
+    if (hipEventElapsedTime(&ms, e0, e1) != hipSuccess) ms = -1.f;
+    *fill_ms = ms;
+  }
+  if (t_opt) *t_opt = hs.t_sel;
+  if (m_opt) *m_opt = hs.t_sel >= 0 ? hs.m_sel : -1;
+  return finish(hs.t_sel >= 0 ? RC_OK : RC_INFEASIBLE);
+}
+
 int rc_family_sets(rc_family f, uint64_t* bits_host, void* stream) {
   if (!f || !bits_host) return RC_E_ARG;
   const int words = f->g->words;

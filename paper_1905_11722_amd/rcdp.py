@@ -93,6 +93,9 @@ def load_library():
                                    ctypes.c_void_p]
     lib.rc_min_budget.restype = ctypes.c_int
     lib.rc_min_budget.argtypes = [P, ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64)]
+    lib.rc_solve_dual.restype = ctypes.c_int
+    lib.rc_solve_dual.argtypes = [P, i64, i32, P, ctypes.POINTER(i64), ctypes.POINTER(i64),
+                                  ctypes.POINTER(ctypes.c_float)]
     lib.rc_solution_fill_kernel_ms.restype = ctypes.c_int
     lib.rc_solution_fill_kernel_ms.argtypes = [P, ctypes.POINTER(ctypes.c_float)]
     lib.rc_reconstruct.restype = ctypes.c_int
@@ -243,6 +246,16 @@ class Family:
         b = ctypes.c_int64(-1)
         _check(load_library().rc_min_budget(self._h, _stream(), ctypes.byref(b)), "rc_min_budget")
         return b.value
+
+    def solve_dual(self, B, objective="tc"):
+        """(t, m, fill_ms) from the memory-indexed table (rc_solve_dual): t* and
+        opt[V, t*] as rc_solve finds them, (-1, -1) when infeasible."""
+        t, m, ms = ctypes.c_int64(-1), ctypes.c_int64(-1), ctypes.c_float(-1.0)
+        st = load_library().rc_solve_dual(self._h, int(B), OBJECTIVES.get(objective, objective),
+                                          _stream(), ctypes.byref(t), ctypes.byref(m),
+                                          ctypes.byref(ms))
+        _check(st, "rc_solve_dual", allow=(OK, INFEASIBLE))
+        return t.value, m.value, ms.value
 
     def sweep(self, budgets, objective="mc"):
         """Solve at every budget in one batched fill (rc_solve_batch):
