@@ -535,7 +535,20 @@ int rc_solve_dual(rc_family f, int64_t B, int32_t objective, void* stream, int64
   if (!D || !dst) return finish(RC_E_NOMEM);
   if (fill_ms && (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess))
     return finish(RC_E_DEVICE);
-  const hipError_t le = launch_dual(f, (int32_t)Beff, (int32_t)W, objective, D, dst, e0, e1, s);
+  // the most pairs of a target per size level: the pair runs of each launch
+  std::vector<int64_t> pp(f->F + 1), level_pairs;
+  if (hipMemcpyAsync(pp.data(), f->pred_ptr, sizeof(int64_t) * pp.size(), hipMemcpyDeviceToHost,
+                     s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return finish(RC_E_DEVICE);
+  for (size_t l = 0; l + 1 < f->level_ptr.size(); l++) {
+    int64_t most = 0;
+    for (int64_t j = f->level_ptr[l]; j < f->level_ptr[l + 1]; j++)
+      most = std::max(most, pp[j + 1] - pp[j]);
+    level_pairs.push_back(most);
+  }
+  const hipError_t le =
+      launch_dual(f, level_pairs, (int32_t)Beff, (int32_t)W, objective, D, dst, e0, e1, s);
   if (le != hipSuccess) {
     set_last_error("dual table launch", le);
     return finish(RC_E_DEVICE);

@@ -276,10 +276,12 @@ size_t min_budget_scratch_bytes(rc_family f, int32_t hi0);
 hipError_t launch_min_budget(rc_family f, int32_t hi0, uint32_t* scratch, hipStream_t s);
 // Memory-indexed table of Algorithm 1's recursion (dual.hip): D[F * W]
 // uint32, W = min(B, M(V)) + 1; t and the least m of the objective into
-// st->t_sel / st->m_sel (-1 when no chain reaches V).  e0/e1 (may be null)
-// are recorded around the table's launches.
-hipError_t launch_dual(rc_family f, int32_t B, int32_t W, int objective, uint32_t* D,
-                       DevStatus* st, hipEvent_t e0, hipEvent_t e1, hipStream_t s);
+// st->t_sel / st->m_sel (-1 when no chain reaches V).  level_pairs[l]: the
+// most pairs of a target of size level l.  e0/e1 (may be null) are recorded
+// around the table's launches.
+hipError_t launch_dual(rc_family f, const std::vector<int64_t>& level_pairs, int32_t B, int32_t W,
+                       int objective, uint32_t* D, DevStatus* st, hipEvent_t e0, hipEvent_t e1,
+                       hipStream_t s);
 int64_t blocked_columns(rc_family f);
 hipError_t launch_fill_blocked(rc_solution sol, hipStream_t s);
 
