@@ -152,6 +152,44 @@ def mc_sweep(rcdp, torch, name="resnet50", count=32, reps=2):
     return best
 
 
+def dual_tables(rcdp, torch, reps=5):
+    """rc_solve_dual on every workload: t* and opt[V, t*] from the table
+    indexed by cached memory.  step_ms = rc_build_family + rc_solve_dual
+    (the whole path to t*, no schedule), fill_ms = its table kernels;
+    `agrees` records that (t*, opt[V, t*]) equals rc_solve's on the same
+    family."""
+    from paper_1905_11722_amd import workloads
+    out = {}
+    for name in workloads.CASES:
+        case = workloads.case(name)
+        g = rcdp.Graph.create(case.graph)
+        steps, fills = [], []
+        fam = None
+        for r in range(reps + 1):
+            if fam is not None:
+                fam.free()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            fam = g.build_family(case.mode)
+            t, m, ms = fam.solve_dual(case.B, case.objective)
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            if r > 0:
+                steps.append((t1 - t0) * 1e3)
+                fills.append(ms)
+        sol = fam.solve(case.B, case.objective)
+        agrees = (t, m) == (sol.t_star, sol.m_star)
+        sol.free()
+        width = min(case.B, 2 * sum(case.graph.M), sum(case.graph.M)) + 1
+        out[name] = {"step_ms": round(sorted(steps)[len(steps) // 2], 4),
+                     "fill_ms": round(sorted(fills)[len(fills) // 2], 4),
+                     "cells": fam.info["num_sets"] * width, "t_star": t, "m_star": m,
+                     "agrees": agrees}
+        fam.free()
+        g.free()
+    return out
+
+
 def workloads_case(name):
     from paper_1905_11722_amd import workloads
     return workloads.case(name)
@@ -242,6 +280,7 @@ def main():
             }
 
     sweep = None if args.no_other_graphs else mc_sweep(rcdp, torch)
+    dual = None if args.no_other_graphs else dual_tables(rcdp, torch)
 
     out = {
         "metric": "DP cell relaxations/sec (whole step: family + fill + traceback)",
@@ -292,6 +331,7 @@ def main():
         },
         "per_graph": per_graph,
         "mc_sweep": sweep,
+        "dual": dual,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(case, W)
