@@ -152,7 +152,7 @@ def mc_sweep(rcdp, torch, name="resnet50", count=32, reps=2):
     return best
 
 
-def dual_tables(rcdp, torch, reps=5):
+def dual_tables(rcdp, torch, reps=5, names=None):
     """rc_solve_dual on every workload: t* and opt[V, t*] from the table
     indexed by cached memory.  step_ms = rc_build_family + rc_solve_dual
     (the whole path to t*, no schedule), fill_ms = its table kernels;
@@ -160,7 +160,7 @@ def dual_tables(rcdp, torch, reps=5):
     family."""
     from paper_1905_11722_amd import workloads
     out = {}
-    for name in workloads.CASES:
+    for name in names or workloads.CASES:
         case = workloads.case(name)
         g = rcdp.Graph.create(case.graph)
         steps, fills = [], []
@@ -236,6 +236,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-other-graphs", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
+    ap.add_argument("--dual", action="store_true",
+                    help="time only the memory-indexed table (rc_solve_dual) on --workload")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
@@ -252,6 +254,10 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     rcdp.load_library()
+    if args.dual:
+        res = dual_tables(rcdp, torch, reps=max(3, args.steps), names=[args.workload])
+        print(json.dumps({"dual": res}), flush=True)
+        return
 
     case = workloads.case(args.workload)
     main_res = time_case(rcdp, torch, case, args.steps, args.warmup)
