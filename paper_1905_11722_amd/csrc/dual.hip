@@ -32,8 +32,8 @@ namespace rcdp {
 namespace {
 
 constexpr int kDualThreads = 256;
-constexpr int kDualPairs = 16;                      // pairs per block
-constexpr int kDualBatch = 8;                       // source loads in flight per thread
+constexpr int kDualPairs = 4;                       // pairs per block
+constexpr int kDualBatch = 4;                       // source loads in flight per thread
 constexpr uint32_t kDualNone = 0xFFFFFFFFu;
 
 __global__ void k_dual_init(uint32_t* D, int64_t cells, int tc, DevStatus* st) {
