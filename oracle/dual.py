@@ -92,10 +92,12 @@ def _lower_sets(succ, order):
 
 
 def family(g, mode):
-    """The family as a bool array [F, n], in ascending size (ties in any
-    order: the optimum does not depend on it).  mode "pruned": the ancestor
-    closures plus the empty set and V (Section 4.3); "exact": every lower
-    set (Section 4.2), by enumeration, for small graphs only."""
+    """The family as a bool array [F, n] in the canonical order: ascending
+    size, equal sizes by ascending numeric value sum of 2^v over the set
+    (the order Algorithm 1's loop takes; the optimum does not depend on it,
+    the traced chain's tie rule does).  mode "pruned": the ancestor closures
+    plus the empty set and V (Section 4.3); "exact": every lower set
+    (Section 4.2), by enumeration, for small graphs only."""
     n = g.n
     succ = _adjacency(g)
     order = _topo(succ)
@@ -113,15 +115,48 @@ def family(g, mode):
         if key not in seen:
             seen.add(key)
             out.append(L)
-    out.sort(key=lambda L: int(L.sum()))
+    out.sort(key=lambda L: (int(L.sum()), sum(1 << int(v) for v in np.flatnonzero(L))))
     return np.array(out, dtype=bool).reshape(len(out), n), succ
 
 
-def solve(g, mode, B, objective="tc"):
-    """(t, m) of the objective, or None when no chain reaches V within B.
+def evaluate_chain(g, S, chain):
+    r"""Eq. 1 and Eq. 2 of the canonical strategy of the chain L_1 < ... < L_k
+    (family indices into S), from their definitions (Section 3): V_i =
+    L_i \ L_{i-1}, U_i = U_{i-1} + boundary(L_i); segment i needs
+    M(U_{i-1}) + 2 M(V_i) + M(delta+(L_i) \ L_i) + M(delta-(delta+(L_i)) \ L_i);
+    the overhead is T(V \ U_k).  Returns (seg, cached, overhead, peak, M(U_k))."""
+    n = g.n
+    succ = _adjacency(g)
+    pred = succ.T
+    T = np.asarray(g.T, dtype=np.int64)
+    M = np.asarray(g.M, dtype=np.int64)
+    seg = np.full(n, -1, dtype=np.int32)
+    U = np.zeros(n, dtype=bool)
+    prev = np.zeros(n, dtype=bool)
+    peak = 0
+    for i, idx in enumerate(chain):
+        L = S[idx]
+        Vi = L & ~prev
+        seg[Vi] = i
+        dp = succ[L].any(axis=0) if L.any() else np.zeros(n, bool)
+        dmdp = pred[dp].any(axis=0) if dp.any() else np.zeros(n, bool)
+        mem = M[U].sum() + 2 * M[Vi].sum() + M[dp & ~L].sum() + M[dmdp & ~L].sum()
+        peak = max(peak, int(mem))
+        U |= L & succ[:, ~L].any(axis=1)
+        prev = L
+    return seg, U.copy(), int(T[~U].sum()), peak, int(M[U].sum())
 
-    Returns a dict with t, m, the family size, the number of pairs and the
-    relaxations done (one per (pair, m) with m inside the budget window)."""
+
+def solve(g, mode, B, objective="tc"):
+    """(t, m) of the objective, or None when no chain reaches V within B,
+    and a chain that attains it.
+
+    Returns a dict with t, m, the family size, the number of pairs, the
+    relaxations done (one per (pair, m) with m inside the budget window) and,
+    when feasible, the chain traced back through the table (from (V, m, t):
+    the smallest family index L whose cell (L, m - dm) passes the budget test
+    and holds t - dt; along an optimal chain one always does) with its seg,
+    cached, overhead, peak and M(U_k) re-evaluated by evaluate_chain."""
     if B < 0:
         raise ValueError("B < 0")
     S, succ = family(g, mode)
@@ -143,19 +178,24 @@ def solve(g, mode, B, objective="tc"):
     unreached = INF if tc else -1
     D = np.full((F, width), unreached, dtype=np.int64)
     D[0, 0] = 0                                                       # (empty set, t = 0, m = 0)
+    def pair(i, j):
+        """c, dt, dm of the pair L < L' (None unless L is a proper subset)."""
+        L, Lp = S[i], S[j]
+        if not (Lp & ~L).any() or (L & ~Lp).any():
+            return None
+        Vp = Lp & ~L
+        return (int(2 * M[Vp].sum() + out[j]), int(T[Vp & ~bd[j]].sum()),
+                int(M[bd[j] & ~L].sum()))
+
     pairs = 0
     relax = 0
     for i in range(F):                   # sources in ascending size: every proper subset first
-        L = S[i]
         for j in range(F):
-            Lp = S[j]
-            if not (Lp & ~L).any() or (L & ~Lp).any():
-                continue                 # L must be a proper subset of L'
+            q = pair(i, j)
+            if q is None:
+                continue
             pairs += 1
-            Vp = Lp & ~L
-            c = 2 * M[Vp].sum() + out[j]
-            dT = T[Vp & ~bd[j]].sum()
-            dM = M[bd[j] & ~L].sum()
+            c, dT, dM = q
             # source m with m + c <= B; also m + dM <= M(V), which every
             # reachable m meets (m = M(U) with U inside L, disjoint from the
             # added boundary), so the clip drops no reachable state
@@ -180,4 +220,28 @@ def solve(g, mode, B, objective="tc"):
     t = int(row[reach].min()) if tc else int(row[reach].max())
     m = int(np.flatnonzero(row == t)[0])
     result.update(t=t, m=m)
+    chain = []
+    j, mj, tj = F - 1, m, t
+    while j != 0:
+        step = None
+        for i in range(F):
+            q = pair(i, j)
+            if q is None:
+                continue
+            c, dT, dM = q
+            ms = mj - dM
+            if ms < 0 or ms > B - c or ms >= width:
+                continue
+            v = int(D[i, ms])
+            if (v < INF if tc else v >= 0) and v + dT == tj:
+                step = (i, ms, v)
+                break
+        assert step is not None, "no predecessor reproduces the cell"
+        chain.append(j)
+        j, mj, tj = step
+    assert (mj, tj) == (0, 0), "the chain must start at (empty set, 0, 0)"
+    chain = chain[::-1]
+    seg, cached, overhead, peak, cache_mem = evaluate_chain(g, S, chain)
+    result.update(chain=chain, seg=seg, cached=cached, overhead=overhead, peak=peak,
+                  cache_mem=cache_mem)
     return result

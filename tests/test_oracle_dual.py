@@ -85,10 +85,10 @@ def test_work_is_the_budget_window():
 
 MUTANTS = [
     ("top = min(B - c, width - 1 - dM)", "top = min(B, width - 1 - dM)"),          # no budget test
-    ("c = 2 * M[Vp].sum() + out[j]", "c = M[Vp].sum() + out[j]"),                  # Eq. 2 term (ii) once
-    ("c = 2 * M[Vp].sum() + out[j]", "c = 2 * M[Vp].sum()"),                       # terms (iii), (iv) dropped
-    ("dT = T[Vp & ~bd[j]].sum()", "dT = T[Vp].sum()"),                            # boundary not excluded
-    ("dM = M[bd[j] & ~L].sum()", "dM = M[bd[j]].sum()"),                          # boundary counted twice
+    ("int(2 * M[Vp].sum() + out[j])", "int(M[Vp].sum() + out[j])"),               # Eq. 2 term (ii) once
+    ("int(2 * M[Vp].sum() + out[j])", "int(2 * M[Vp].sum())"),                    # terms (iii), (iv) dropped
+    ("int(T[Vp & ~bd[j]].sum())", "int(T[Vp].sum())"),                            # boundary not excluded
+    ("int(M[bd[j] & ~L].sum())", "int(M[bd[j]].sum())"),                          # boundary counted twice
     ("out[j] = M[dp & ~L].sum() + M[dmdp & ~L].sum()", "out[j] = M[dp & ~L].sum()"),
     ("m = int(np.flatnonzero(row == t)[0])", "m = int(np.flatnonzero(row == t)[-1])"),
     ("np.maximum(dst, cand, out=dst)", "np.minimum(dst, np.where(cand < 0, INF, cand), out=dst)"),
@@ -115,6 +115,11 @@ def test_planted_mistakes_are_caught(oracle_mod, k):
                     try:
                         got = mod.solve(g, mode, B, objective)
                         got = (got["t"], got["m"])
+                        if got[0] is not None:
+                            r = mod.solve(g, mode, B, objective)
+                            if (r["overhead"], r["cache_mem"]) != got or r["peak"] > B:
+                                caught = True
+                                break
                     except Exception:
                         caught = True
                         break
@@ -128,3 +133,72 @@ def test_planted_mistakes_are_caught(oracle_mod, k):
         if caught:
             break
     assert caught, MUTANTS[k]
+
+
+EVAL_MUTANTS = [
+    ("mem = M[U].sum() + 2 * M[Vi].sum()", "mem = M[U].sum() + M[Vi].sum()"),
+    ("U |= L & succ[:, ~L].any(axis=1)", "U |= L"),
+    ("return seg, U.copy(), int(T[~U].sum())", "return seg, U.copy(), int(T[U].sum())"),
+    ("Vi = L & ~prev", "Vi = L"),
+]
+
+
+def _chain_checks(oracle_mod, g, mode, B, objective, mod=dual):
+    """The traced chain re-evaluates to the optimum (Eq. 1 overhead = t*,
+    M(U_k) = opt[V, t*], every segment within B), and its evaluation equals
+    the C oracle's evaluation of the same chain."""
+    d = mod.solve(g, mode, B, objective)
+    if d["t"] is None:
+        return True
+    if (d["overhead"], d["cache_mem"]) != (d["t"], d["m"]) or d["peak"] > B:
+        return False
+    ref = oracle_mod.solve(g, mode, B, objective)
+    return ref.evaluate_chain(d["chain"]) == (d["overhead"], d["peak"], d["cache_mem"])
+
+
+@pytest.mark.parametrize("seed", range(12))
+@pytest.mark.parametrize("mode", ["exact", "pruned"])
+def test_traced_chain_reevaluates_to_the_optimum(oracle_mod, seed, mode):
+    g = W.random_dag(9, 0.35, seed)
+    for objective in ("tc", "mc"):
+        for B in BUDGETS:
+            assert _chain_checks(oracle_mod, g, mode, B, objective), (seed, mode, objective, B)
+
+
+@pytest.mark.parametrize("name", ["chain16", "ladder40", "resnet50_t10", "unet_t10"])
+def test_traced_chain_workloads(oracle_mod, name):
+    c = W.case(name)
+    for objective in ("tc", "mc"):
+        assert _chain_checks(oracle_mod, c.graph, c.mode, c.B, objective), (name, objective)
+
+
+def test_family_order_is_canonical(oracle_mod):
+    """Same members in the same order as the C oracle (ascending size, then
+    ascending sum of 2^v), so that chains are comparable index by index."""
+    for seed in range(6):
+        g = W.random_dag(8, 0.3, seed)
+        for mode in ("exact", "pruned"):
+            S, _ = dual.family(g, mode)
+            ref = oracle_mod.solve(g, mode, 10 ** 6, "tc").sets()
+            assert S.shape == ref.shape and (S == ref).all(), (seed, mode)
+
+
+@pytest.mark.parametrize("k", range(len(EVAL_MUTANTS)))
+def test_planted_evaluation_mistakes_are_caught(oracle_mod, k):
+    import inspect
+    import types
+    src = inspect.getsource(dual)
+    a, b = EVAL_MUTANTS[k]
+    assert src.count(a) == 1
+    mod = types.ModuleType("dual_eval_mutant")
+    exec(compile(src.replace(a, b), "dual_eval_mutant", "exec"), mod.__dict__)
+    caught = False
+    for seed in range(12):
+        g = W.random_dag(9, 0.35, seed)
+        for B in BUDGETS:
+            if not _chain_checks(oracle_mod, g, "exact", B, "tc", mod):
+                caught = True
+                break
+        if caught:
+            break
+    assert caught, EVAL_MUTANTS[k]
