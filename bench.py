@@ -153,11 +153,12 @@ def mc_sweep(rcdp, torch, name="resnet50", count=32, reps=2):
 
 
 def dual_tables(rcdp, torch, reps=5, names=None):
-    """rc_solve_dual on every workload: t* and opt[V, t*] from the table
-    indexed by cached memory.  step_ms = rc_build_family + rc_solve_dual
-    (the whole path to t*, no schedule), fill_ms = its table kernels;
-    `agrees` records that (t*, opt[V, t*]) equals rc_solve's on the same
-    family."""
+    """rc_solve_dual on every workload: t*, opt[V, t*] and a schedule from
+    the table indexed by cached memory.  step_ms = rc_build_family +
+    rc_solve_dual with its schedule (the same outputs as a step of the
+    time-indexed path: t*, chain, Eq. 1 / Eq. 2), fill_ms = its table
+    kernels; `agrees` records that (t*, opt[V, t*]) equals rc_solve's on the
+    same family and that the schedule re-evaluates to them."""
     from paper_1905_11722_amd import workloads
     out = {}
     for name in names or workloads.CASES:
@@ -171,14 +172,15 @@ def dual_tables(rcdp, torch, reps=5, names=None):
             torch.cuda.synchronize()
             t0 = time.perf_counter()
             fam = g.build_family(case.mode)
-            t, m, ms = fam.solve_dual(case.B, case.objective)
+            t, m, ms, sched = fam.solve_dual(case.B, case.objective, schedule=True)
             torch.cuda.synchronize()
             t1 = time.perf_counter()
             if r > 0:
                 steps.append((t1 - t0) * 1e3)
                 fills.append(ms)
         sol = fam.solve(case.B, case.objective)
-        agrees = (t, m) == (sol.t_star, sol.m_star)
+        agrees = (t, m) == (sol.t_star, sol.m_star) and (
+            sched is None or (sched.overhead, sched.cache_mem) == (t, m))
         sol.free()
         width = min(case.B, 2 * sum(case.graph.M), sum(case.graph.M)) + 1
         out[name] = {"step_ms": round(sorted(steps)[len(steps) // 2], 4),

@@ -145,25 +145,35 @@ int rc_family_sets(rc_family f, uint64_t* bits_host, void* stream);
  */
 int rc_min_budget(rc_family f, void* stream, int64_t* B_min);
 /*
- * rc_solve_dual -- t* and opt[V, t*] of rc_solve from a table indexed by
- * cached memory instead of time.  Algorithm 1 (Section 4.2, Appendix A)
- * moves a chain state (L, t, m) along a pair L < L' to (L', t + dt, m + dm)
- * when m + c <= B, a test on m alone; this table keeps, per (L, m) with
- * m in [0, min(B, M(V))], the least t (RC_TIME_CENTRIC) or the greatest t
- * (RC_MEMORY_CENTRIC, Section 4.4) over the chains reaching that state.
- * Its rows have min(B, M(V)) + 1 cells instead of T(L \ boundary(L)) + 1,
- * and its optimum over row V equals rc_solve's: *t_opt = t*, *m_opt = the
- * least m attaining it = opt[V, t*] (both -1 when infeasible).  No table or
- * schedule is kept (rc_solve and rc_reconstruct give those).
+ * rc_solve_dual -- t* and opt[V, t*] of rc_solve, and a schedule attaining
+ * them, from a table indexed by cached memory instead of time.  Algorithm 1
+ * (Section 4.2, Appendix A) moves a chain state (L, t, m) along a pair
+ * L < L' to (L', t + dt, m + dm) when m + c <= B, a test on m alone; this
+ * table keeps, per (L, m) with m in [0, min(B, M(V))], the least t
+ * (RC_TIME_CENTRIC) or the greatest t (RC_MEMORY_CENTRIC, Section 4.4) over
+ * the chains reaching that state.  Its rows have min(B, M(V)) + 1 cells
+ * instead of T(L \ boundary(L)) + 1, and its optimum over row V equals
+ * rc_solve's: *t_opt = t*, *m_opt = the least m attaining it = opt[V, t*]
+ * (both -1 when infeasible).
  *  B >= 0 as rc_solve.  *fill_ms (may be NULL): milliseconds between HIP
- *  events around the table's kernels.  Synchronises stream; device memory
- *  comes from the family's allocator and is returned before the call ends.
+ *  events around the table's kernels.
+ *  Schedule (computed only if one of these is non-NULL and B is feasible):
+ *  the chain traced back through the table -- from (V, m*, t*) the smallest
+ *  family index L whose cell (L, m - dm) passes the budget test and holds
+ *  t - dt -- re-evaluated from Section 3's definitions; *k, chain_host[num
+ *  sets], seg_host[n], cached_host[n], *overhead (Eq. 1, = t*), *peak (Eq. 2,
+ *  <= B), *cache_mem (M(U_k) = opt[V, t*]) as rc_reconstruct.  Among equally
+ *  good chains it may pick another than rc_reconstruct.
+ *  Synchronises stream; device memory comes from the family's allocator and
+ *  is returned before the call ends.
  * Returns RC_OK, RC_INFEASIBLE, or RC_E_ARG (NULL family, B < 0, bad
  * objective), RC_E_OVERFLOW (T(V) >= 2^32 - 1, or more than 2^31 cells),
  * RC_E_NOMEM, RC_E_DEVICE.
  */
 int rc_solve_dual(rc_family f, int64_t B, int32_t objective, void* stream, int64_t* t_opt,
-                  int64_t* m_opt, float* fill_ms);
+                  int64_t* m_opt, float* fill_ms, int32_t* k, int32_t* chain_host,
+                  int32_t* seg_host, uint8_t* cached_host, int64_t* overhead, int64_t* peak,
+                  int64_t* cache_mem);
 void rc_family_free(rc_family f);
 
 /*

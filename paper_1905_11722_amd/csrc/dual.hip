@@ -26,6 +26,8 @@
 #include <vector>
 
 #include "rc_internal.h"
+#include "dual.h"
+#include "schedule.h"
 
 namespace rcdp {
 
@@ -125,7 +127,114 @@ __global__ __launch_bounds__(kDualThreads) void k_dual_select(const uint32_t* __
   }
 }
 
+// Traceback through the table (Section 4.2's, read on cells (L, m)): from
+// (V, m*, t*), the next set is the smallest family index L among the pairs
+// L < L' whose cell (L, m - dm) passes the budget test and holds t - dt (one
+// always does along an optimal chain: its state there is reachable, and a
+// better one would give a better optimum).  The walk must end at (empty set,
+// 0, 0); then the chain's strategy is evaluated (finish_schedule).  The
+// pairs of a step are scanned kDualTraceThreads at a time; the first hit in
+// family order is the lowest hitting thread of the first chunk with one.
+constexpr int kDualTraceThreads = 512;
+
+template <bool kTC>
+__global__ __launch_bounds__(kDualTraceThreads) void k_dual_trace(
+    int64_t F, int n, int words, int64_t fstride, const uint64_t* __restrict__ bits,
+    const uint64_t* __restrict__ bd, const int32_t* __restrict__ A, const int32_t* __restrict__ T,
+    const int32_t* __restrict__ M, const int64_t* __restrict__ pred_ptr,
+    const int32_t* __restrict__ pidx, const int32_t* __restrict__ pdt,
+    const int32_t* __restrict__ pdm, const int32_t* __restrict__ pc, int32_t B, int32_t W,
+    const uint32_t* __restrict__ D, int64_t T_total, DevStatus* st, int32_t* chain, int32_t* seg,
+    uint8_t* cached) {
+  constexpr int kWaves = kDualTraceThreads / 64;
+  __shared__ int32_t s_first[2][kWaves];
+  __shared__ int32_t s_src[2][kDualTraceThreads];
+  __shared__ int32_t s_dt[2][kDualTraceThreads];
+  __shared__ int32_t s_dm[2][kDualTraceThreads];
+  __shared__ int32_t s_chain[kMaxNodes + 1];
+  __shared__ int32_t s_M[kMaxNodes];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid / 64;
+  int64_t j = F - 1;
+  int64_t t = st->t_sel, m = st->m_sel;
+  int32_t k = 0;
+  bool bad = t < 0 || m < 0 || m >= W;
+  int par = 0;
+  while (j != 0 && !bad) {
+    if (k >= F || k > n) {                          // each step removes a node
+      bad = true;
+      break;
+    }
+    const int64_t p0 = pred_ptr[j], p1 = pred_ptr[j + 1];
+    int32_t next_i = -1, next_dt = 0, next_dm = 0;
+    for (int64_t base = p0; base < p1 && next_i < 0; base += kDualTraceThreads) {
+      const int64_t p = base + tid;
+      const bool valid = p < p1;
+      const int64_t pq = valid ? p : p0;
+      const int32_t i = pidx[pq], dt = pdt[pq], dm = pdm[pq], c = pc[pq];
+      const int64_t ms = m - dm;                     // memory before the step
+      const bool ok = valid && ms >= 0 && ms <= B - c;
+      const uint32_t x = D[(int64_t)i * W + (ok ? ms : 0)];
+      const bool reached = kTC ? x != kDualNone : x != 0u;
+      const int64_t tx = kTC ? (int64_t)x : (int64_t)x - 1;
+      const bool hit = ok && reached && tx + dt == t;
+      const unsigned long long bal = __ballot(hit);
+      if (lane == 0) s_first[par][wave] = bal ? wave * 64 + __ffsll((long long)bal) - 1 : INT32_MAX;
+      s_src[par][tid] = i;
+      s_dt[par][tid] = dt;
+      s_dm[par][tid] = dm;
+      __syncthreads();
+      int32_t f = INT32_MAX;
+#pragma unroll
+      for (int q = 0; q < kWaves; q++) f = min(f, s_first[par][q]);
+      if (f != INT32_MAX) {
+        next_i = s_src[par][f];
+        next_dt = s_dt[par][f];
+        next_dm = s_dm[par][f];
+      }
+      par ^= 1;
+    }
+    if (next_i < 0) {
+      bad = true;
+      break;
+    }
+    if (tid == 0) chain[k] = (int32_t)j;
+    k++;
+    t -= next_dt;
+    m -= next_dm;
+    j = next_i;
+  }
+  if (t != 0 || m != 0) bad = true;                  // the walk must end at (empty set, 0, 0)
+  __syncthreads();
+  if (bad) {
+    if (tid == 0) {
+      st->error = 2;
+      st->k = -1;
+    }
+    return;
+  }
+  finish_schedule<kDualTraceThreads>(k, n, words, fstride, bits, bd, A, T, M, T_total, st, chain,
+                                     seg, cached, s_chain, s_M);
+}
+
 }  // namespace
+
+hipError_t launch_dual_trace(rc_family f, int32_t B, int32_t W, int objective, const uint32_t* D,
+                             DevStatus* st, int32_t* chain, int32_t* seg, uint8_t* cached,
+                             hipStream_t s) {
+  rc_graph g = f->g;
+  if (objective == RC_TIME_CENTRIC)
+    hipLaunchKernelGGL(k_dual_trace<true>, dim3(1), dim3(kDualTraceThreads), 0, s, f->F, g->n,
+                       g->words, f->fstride, f->bits, f->bd, f->A, g->dT, g->dM, f->pred_ptr,
+                       f->pidx, f->pdt, f->pdm, f->pc, B, W, D, g->T_total, st, chain, seg,
+                       cached);
+  else
+    hipLaunchKernelGGL(k_dual_trace<false>, dim3(1), dim3(kDualTraceThreads), 0, s, f->F, g->n,
+                       g->words, f->fstride, f->bits, f->bd, f->A, g->dT, g->dM, f->pred_ptr,
+                       f->pidx, f->pdt, f->pdm, f->pc, B, W, D, g->T_total, st, chain, seg,
+                       cached);
+  return hipGetLastError();
+}
 
 hipError_t launch_dual(rc_family f, const std::vector<int64_t>& level_pairs, int32_t B, int32_t W,
                        int objective, uint32_t* D, DevStatus* st, hipEvent_t e0, hipEvent_t e1,

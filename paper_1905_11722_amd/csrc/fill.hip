@@ -23,6 +23,7 @@
 #include <algorithm>
 
 #include "rc_internal.h"
+#include "schedule.h"
 
 namespace rcdp {
 
@@ -278,58 +279,8 @@ __global__ __launch_bounds__(kTraceThreads) void k_trace(
     }
     return;
   }
-  // chain in increasing order, kept in LDS as well; node memories in LDS
-  for (int c = tid; c < k; c += kTraceThreads) s_chain[c] = chain[k - 1 - c];
-  for (int v = tid; v < n; v += kTraceThreads) {
-    seg[v] = -1;
-    s_M[v] = M[v];
-  }
-  __syncthreads();
-  for (int c = tid; c < k; c += kTraceThreads) chain[c] = s_chain[c];
-  if (tid >= kWave) return;
-  // Eq. 2 per segment: M(U_{i-1}) + 2 M(V_i) + A(L_i), U grows by the
-  // boundary of each L_i; the loads of kPre chain steps are issued together
-  constexpr int kPre = 16;
-  const bool active = lane < words;
-  uint64_t U = 0, prev = 0;
-  int64_t mu = 0, peak = 0;
-  for (int c0 = 0; c0 < k; c0 += kPre) {
-    uint64_t Ls[kPre], Bs[kPre];
-    int32_t As[kPre];
-#pragma unroll
-    for (int x = 0; x < kPre; x++) {
-      const int c = c0 + x < k ? c0 + x : k - 1;
-      const int64_t sx = s_chain[c];
-      Ls[x] = active ? bits[(int64_t)lane * fstride + sx] : 0ull;
-      Bs[x] = active ? bd[(int64_t)lane * fstride + sx] : 0ull;
-      As[x] = A[sx];
-    }
-#pragma unroll
-    for (int x = 0; x < kPre; x++) {
-      const int c = c0 + x;
-      if (c >= k) break;
-      const uint64_t Vi = Ls[x] & ~prev;
-      const int64_t mv = wave_sum_i64(active ? word_cost(Vi, lane, s_M) : 0);
-      const int64_t mem = mu + 2 * mv + As[x];
-      peak = mem > peak ? mem : peak;
-      for (uint64_t bb = Vi; bb; bb &= bb - 1) seg[lane * 64 + __builtin_ctzll(bb)] = c;
-      const uint64_t add = Bs[x] & ~U;
-      mu += wave_sum_i64(active ? word_cost(add, lane, s_M) : 0);
-      U |= add;
-      prev = Ls[x];
-    }
-  }
-  for (int b = 0; b < 64 && active; b++) {
-    const int v = lane * 64 + b;
-    if (v < n) cached[v] = (uint8_t)((U >> b) & 1ull);
-  }
-  const int64_t tu = wave_sum_i64(active ? word_cost(U, lane, T) : 0);
-  if (lane == 0) {
-    st->k = k;
-    st->overhead = T_total - tu;
-    st->peak = peak;
-    st->cache_mem = mu;
-  }
+  finish_schedule<kTraceThreads>(k, n, words, fstride, bits, bd, A, T, M, T_total, st, chain, seg,
+                                  cached, s_chain, s_M);
 }
 
 }  // namespace

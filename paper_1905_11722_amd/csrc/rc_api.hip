@@ -11,6 +11,7 @@
 #include <vector>
 
 #include "rc_internal.h"
+#include "dual.h"
 
 using namespace rcdp;
 
@@ -509,7 +510,9 @@ int rc_min_budget(rc_family f, void* stream, int64_t* B_min) {
 }
 
 int rc_solve_dual(rc_family f, int64_t B, int32_t objective, void* stream, int64_t* t_opt,
-                  int64_t* m_opt, float* fill_ms) {
+                  int64_t* m_opt, float* fill_ms, int32_t* k, int32_t* chain_host,
+                  int32_t* seg_host, uint8_t* cached_host, int64_t* overhead, int64_t* peak,
+                  int64_t* cache_mem) {
   if (!f || B < 0) return RC_E_ARG;
   if (objective != RC_TIME_CENTRIC && objective != RC_MEMORY_CENTRIC) return RC_E_ARG;
   const int64_t Beff = std::min<int64_t>(B, 2 * f->g->M_total);
@@ -557,6 +560,43 @@ int rc_solve_dual(rc_family f, int64_t B, int32_t objective, void* stream, int64
   if (hipMemcpyAsync(&hs, dst, sizeof(hs), hipMemcpyDeviceToHost, s) != hipSuccess ||
       hipStreamSynchronize(s) != hipSuccess)
     return finish(RC_E_DEVICE);
+  const bool schedule = k || chain_host || seg_host || cached_host || overhead || peak || cache_mem;
+  if (schedule && hs.t_sel >= 0) {
+    const int n = f->g->n;
+    int32_t* chain_d = A.get_n<int32_t>(f->F);
+    int32_t* seg_d = A.get_n<int32_t>(n);
+    uint8_t* cached_d = A.get_n<uint8_t>(n);
+    if (!chain_d || !seg_d || !cached_d) return finish(RC_E_NOMEM);
+    const hipError_t te = launch_dual_trace(f, (int32_t)Beff, (int32_t)W, objective, D, dst,
+                                            chain_d, seg_d, cached_d, s);
+    if (te != hipSuccess) {
+      set_last_error("dual traceback launch", te);
+      return finish(RC_E_DEVICE);
+    }
+    std::vector<int32_t> ch(f->F), sg(n);
+    std::vector<uint8_t> ca(n);
+    DevStatus ts;
+    if (hipMemcpyAsync(&ts, dst, sizeof(ts), hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipMemcpyAsync(ch.data(), chain_d, sizeof(int32_t) * f->F, hipMemcpyDeviceToHost, s) !=
+            hipSuccess ||
+        (n > 0 &&
+         (hipMemcpyAsync(sg.data(), seg_d, sizeof(int32_t) * n, hipMemcpyDeviceToHost, s) !=
+              hipSuccess ||
+          hipMemcpyAsync(ca.data(), cached_d, n, hipMemcpyDeviceToHost, s) != hipSuccess)) ||
+        hipStreamSynchronize(s) != hipSuccess)
+      return finish(RC_E_DEVICE);
+    if (ts.error || ts.k < 0 || ts.k > f->F) {
+      set_last_error_msg("dual traceback: the walk did not end at (empty set, 0, 0)");
+      return finish(RC_E_DEVICE);
+    }
+    if (k) *k = ts.k;
+    if (chain_host) std::copy(ch.begin(), ch.begin() + ts.k, chain_host);
+    if (seg_host) std::copy(sg.begin(), sg.end(), seg_host);
+    if (cached_host) std::copy(ca.begin(), ca.end(), cached_host);
+    if (overhead) *overhead = ts.overhead;
+    if (peak) *peak = ts.peak;
+    if (cache_mem) *cache_mem = ts.cache_mem;
+  }
   if (fill_ms) {
     float ms = -1.f;
     if (hipEventElapsedTime(&ms, e0, e1) != hipSuccess) ms = -1.f;

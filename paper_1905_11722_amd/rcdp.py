@@ -95,7 +95,8 @@ def load_library():
     lib.rc_min_budget.argtypes = [P, ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64)]
     lib.rc_solve_dual.restype = ctypes.c_int
     lib.rc_solve_dual.argtypes = [P, i64, i32, P, ctypes.POINTER(i64), ctypes.POINTER(i64),
-                                  ctypes.POINTER(ctypes.c_float)]
+                                  ctypes.POINTER(ctypes.c_float), ctypes.POINTER(i32), P, P, P,
+                                  ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i64)]
     lib.rc_solution_fill_kernel_ms.restype = ctypes.c_int
     lib.rc_solution_fill_kernel_ms.argtypes = [P, ctypes.POINTER(ctypes.c_float)]
     lib.rc_reconstruct.restype = ctypes.c_int
@@ -247,15 +248,36 @@ class Family:
         _check(load_library().rc_min_budget(self._h, _stream(), ctypes.byref(b)), "rc_min_budget")
         return b.value
 
-    def solve_dual(self, B, objective="tc"):
+    def solve_dual(self, B, objective="tc", schedule=False):
         """(t, m, fill_ms) from the memory-indexed table (rc_solve_dual): t* and
-        opt[V, t*] as rc_solve finds them, (-1, -1) when infeasible."""
+        opt[V, t*] as rc_solve finds them, (-1, -1) when infeasible.  With
+        schedule=True, (t, m, fill_ms, Schedule or None): the chain traced back
+        through that table and its re-evaluated strategy."""
+        lib = load_library()
         t, m, ms = ctypes.c_int64(-1), ctypes.c_int64(-1), ctypes.c_float(-1.0)
-        st = load_library().rc_solve_dual(self._h, int(B), OBJECTIVES.get(objective, objective),
-                                          _stream(), ctypes.byref(t), ctypes.byref(m),
-                                          ctypes.byref(ms))
+        if not schedule:
+            st = lib.rc_solve_dual(self._h, int(B), OBJECTIVES.get(objective, objective),
+                                   _stream(), ctypes.byref(t), ctypes.byref(m), ctypes.byref(ms),
+                                   None, None, None, None, None, None, None)
+            _check(st, "rc_solve_dual", allow=(OK, INFEASIBLE))
+            return t.value, m.value, ms.value
+        F = self.info["num_sets"]
+        n = self.graph.n
+        k = ctypes.c_int32(-1)
+        chain = np.zeros(max(F, 1), dtype=np.int32)
+        seg = np.zeros(max(n, 1), dtype=np.int32)
+        cached = np.zeros(max(n, 1), dtype=np.uint8)
+        o, p, c = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+        st = lib.rc_solve_dual(self._h, int(B), OBJECTIVES.get(objective, objective), _stream(),
+                               ctypes.byref(t), ctypes.byref(m), ctypes.byref(ms), ctypes.byref(k),
+                               chain.ctypes.data, seg.ctypes.data, cached.ctypes.data,
+                               ctypes.byref(o), ctypes.byref(p), ctypes.byref(c))
         _check(st, "rc_solve_dual", allow=(OK, INFEASIBLE))
-        return t.value, m.value, ms.value
+        if st == INFEASIBLE:
+            return t.value, m.value, ms.value, None
+        return t.value, m.value, ms.value, Schedule(
+            chain[:k.value].copy(), seg[:n].copy(), cached[:n].astype(bool), o.value, p.value,
+            c.value)
 
     def sweep(self, budgets, objective="mc"):
         """Solve at every budget in one batched fill (rc_solve_batch):

@@ -4,8 +4,12 @@ rc_solve_dual must return exactly Algorithm 1's t* and opt[V, t*]: checked
 against the memory-indexed oracle (oracle/dual.py, pinned to the C oracle
 and to brute force) and against rc_solve on the same family, for both
 objectives, both families, budgets from below the feasibility threshold to
-unconstrained, and the degenerate graphs.
+unconstrained, and the degenerate graphs.  The chain traced back through the
+table, its seg / cached and its Eq. 1 / Eq. 2 re-evaluation must equal the
+oracle's bit for bit (same family order, same tie rule).
 """
+
+import numpy as np
 
 import pytest
 
@@ -33,8 +37,20 @@ def check(rc, g, mode, budgets, objectives=("tc", "mc"), against_solve=True):
     fam = rc.Graph.create(g).build_family(mode)
     for B in budgets:
         for objective in objectives:
+            d = dual.solve(g, mode, B, objective)
             t, m, ms = fam.solve_dual(B, objective)
-            assert (t, m) == _expect(dual.solve(g, mode, B, objective)), (mode, B, objective)
+            assert (t, m) == _expect(d), (mode, B, objective)
+            t2, m2, _, sched = fam.solve_dual(B, objective, schedule=True)
+            assert (t2, m2) == (t, m)
+            if d["t"] is None:
+                assert sched is None
+            else:
+                np.testing.assert_array_equal(sched.chain, d["chain"])
+                np.testing.assert_array_equal(sched.seg, d["seg"])
+                np.testing.assert_array_equal(sched.cached, d["cached"])
+                assert (sched.overhead, sched.peak, sched.cache_mem) == (
+                    d["overhead"], d["peak"], d["cache_mem"])
+                assert (sched.overhead, sched.cache_mem) == (t, m) and sched.peak <= B
             if against_solve and B <= 60000:
                 sol = fam.solve(B, objective)
                 assert (t, m) == (sol.t_star, sol.m_star), (mode, B, objective)
