@@ -105,3 +105,20 @@ def test_bad_arguments_and_repeat(rc):
     first = fam.solve_dual(c.B, "tc")[:2]
     for _ in range(3):
         assert fam.solve_dual(c.B, "tc")[:2] == first
+
+
+def test_wide_levels_exact_antichain(rc):
+    """An antichain of 15 nodes: the exact family is all 2^15 subsets, with
+    size levels of up to 6435 targets and targets of up to 32767 pairs (many
+    blocks along y and z).  Against rc_solve on the same family (the oracle
+    is too slow here) and by re-evaluating the schedule."""
+    g = W.antichain(15, seed=3)
+    fam = rc.Graph.create(g).build_family("exact")
+    assert fam.info["num_sets"] == 1 << 15
+    for B in (2 * max(g.M), sum(g.M), 2 * sum(g.M)):
+        for objective in ("tc", "mc"):
+            t, m, _, sched = fam.solve_dual(B, objective, schedule=True)
+            sol = fam.solve(B, objective)
+            assert (t, m) == (sol.t_star, sol.m_star), (B, objective)
+            sol.free()
+            assert (sched.overhead, sched.cache_mem) == (t, m) and sched.peak <= B
