@@ -38,7 +38,7 @@ __device__ __forceinline__ int64_t word_cost(uint64_t bits, int word, const int3
 // and st->{k, overhead, peak, cache_mem} are filled.  s_chain[k] and s_M[n]
 // are LDS scratch of the caller.
 template <int kThreads>
-__device__ void finish_schedule(int32_t k, int n, int words, int64_t fstride,
+__device__ __forceinline__ void finish_schedule(int32_t k, int n, int words, int64_t fstride,
                                 const uint64_t* __restrict__ bits, const uint64_t* __restrict__ bd,
                                 const int32_t* __restrict__ A, const int32_t* __restrict__ T,
                                 const int32_t* __restrict__ M, int64_t T_total, DevStatus* st,
