@@ -22,8 +22,16 @@ and opt[V, t*] of Algorithm 1 is the least m with tmin[V, m] = t* (resp.
 tmax[V, m] = t_MC).  Rows run over m in [0, min(B, M(V))]: every cached
 memory is a sum of distinct node memories (m = M(U), U a subset of V).
 
-Pinned by tests/test_oracle_dual.py against Algorithm 1 (the C oracle) and
-against brute force over every chain (tests/bruteforce.py).
+A chain attaining the optimum is traced back through the table (Section
+4.2's traceback read on cells (L, m)) and re-evaluated from the definitions
+of Section 3 (evaluate_chain).
+
+Pinned by tests/test_oracle_dual.py: t* and opt[V, t*] against Algorithm 1
+(the C oracle) and against brute force over every chain
+(tests/bruteforce.py); the traced chain by its re-evaluation (overhead = t*,
+M(U_k) = opt[V, t*], every segment within B) and by the C oracle's
+evaluation of the same chain; the family order against the C oracle's; and
+planted mistakes in the table and in the evaluation.
 """
 
 import numpy as np
