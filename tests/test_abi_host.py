@@ -71,3 +71,18 @@ def test_null_handles():
     lib.rc_graph_free(None)
     lib.rc_family_free(None)
     lib.rc_solution_free(None)
+
+
+def test_header_is_plain_c(tmp_path):
+    """include/rc.h is a C ABI: it compiles as strict C99 with every warning."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("no C compiler")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    src = tmp_path / "use_rc.c"
+    src.write_text('#include "rc.h"\nint main(void) { return (int)sizeof(rc_family_info); }\n')
+    r = subprocess.run(["gcc", "-std=c99", "-Wall", "-Wextra", "-pedantic", "-Werror",
+                        "-fsyntax-only", "-I", os.path.join(root, "include"), str(src)],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
