@@ -40,6 +40,9 @@ def open_library(path):
     lib.oracle_solve.restype = P
     lib.oracle_solve.argtypes = [ctypes.c_int, i32p, i32p, i64p, i64p, ctypes.c_int,
                                  ctypes.c_int64, ctypes.c_int, ctypes.c_int64, ctypes.c_int64]
+    lib.oracle_solve_dominance.restype = P
+    lib.oracle_solve_dominance.argtypes = [ctypes.c_int, i32p, i32p, i64p, i64p, ctypes.c_int,
+                                           ctypes.c_int64, ctypes.c_int64]
     for name, rt in [("oracle_status", ctypes.c_int), ("oracle_num_sets", ctypes.c_int64),
                      ("oracle_T_total", ctypes.c_int64), ("oracle_num_pairs", ctypes.c_int64),
                      ("oracle_relaxations_literal", ctypes.c_int64),
@@ -166,6 +169,23 @@ def solve(graph, mode, B, objective="tc", max_sets=1 << 20, max_sources=-1, csr=
                          int(max_sets), int(max_sources))
     if not h:
         raise MemoryError("oracle_solve returned NULL")
+    return OracleResult(graph, h)
+
+
+def solve_dominance(graph, mode, B, max_sets=1 << 20):
+    """Algorithm 1 with the dominance skip of Section 4.2's last paragraph
+    (time-centric only): the same t* and opt[V, t*], a table whose entries
+    are never below solve()'s."""
+    lib = _load()
+    row_ptr, col_idx = graph.csr()
+    rp, ci = _arr(row_ptr, np.int32), _arr(col_idx, np.int32)
+    Ta, Ma = _arr(graph.T, np.int64), _arr(graph.M, np.int64)
+    h = lib.oracle_solve_dominance(graph.n, _ptr(rp, ctypes.c_int32), _ptr(ci, ctypes.c_int32),
+                                   _ptr(Ta, ctypes.c_int64), _ptr(Ma, ctypes.c_int64),
+                                   MODES[mode] if isinstance(mode, str) else mode, int(B),
+                                   int(max_sets))
+    if not h:
+        raise MemoryError("oracle_solve_dominance returned NULL")
     return OracleResult(graph, h)
 
 

@@ -20,7 +20,10 @@
  * optarg table and both objectives; the closed form of chain graphs; the
  * floor T(Sinks) and ceiling T(V) of the objectives; infeasibility below
  * 2 max M_v; monotonicity in B; pruned >= exact; the t-free row-minimum
- * DP; re-evaluation of the returned schedule with Eq. 1 / Eq. 2.
+ * DP; re-evaluation of the returned schedule with Eq. 1 / Eq. 2.  The
+ * dominance skip (oracle_solve_dominance) against its closed form from the
+ * brute-force table: every row keeps its weak front, and each cell is the
+ * least one-step extension of the source rows' fronts.
  *
  * Readings of the paper taken here (each one is listed with its reason in
  * the design notes):
@@ -36,6 +39,9 @@
  *    the selection of t in row V; the table is the same.
  *  - optarg keeps the predecessor's family index; its t is recovered as
  *    t' - T(V' \ boundary(L')).
+ *  - The dominance skip (Section 4.2, last paragraph) compares each entry
+ *    with the least of the same row's earlier entries, strictly, and is
+ *    offered for the time-centric objective only.
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -319,9 +325,10 @@ void oracle_free(oracle_result* r);
  * outer loop; otherwise only its first max_sources iterations (used to time
  * a bounded sample; the selection step is then skipped).
  */
-oracle_result* oracle_solve(int n, const int32_t* row_ptr, const int32_t* col_idx,
-                            const int64_t* T, const int64_t* M, int mode, int64_t B,
-                            int objective, int64_t max_sets, int64_t max_sources) {
+static oracle_result* solve_impl(int n, const int32_t* row_ptr, const int32_t* col_idx,
+                                 const int64_t* T, const int64_t* M, int mode, int64_t B,
+                                 int objective, int64_t max_sets, int64_t max_sources,
+                                 int dominance_skip) {
   oracle_result* r = (oracle_result*)calloc(1, sizeof(oracle_result));
   if (!r) return NULL;
   r->n = n;
@@ -331,7 +338,8 @@ oracle_result* oracle_solve(int n, const int32_t* row_ptr, const int32_t* col_id
   memset(&g, 0, sizeof(g));
   int* topo = (int*)malloc(sizeof(int) * (n + 1));
   if (!topo) { r->status = ORC_E_NOMEM; return r; }
-  int st = (mode != 0 && mode != 1) || B < 0 || (objective != 0 && objective != 1)
+  int st = (mode != 0 && mode != 1) || B < 0 || (objective != 0 && objective != 1) ||
+                   (dominance_skip && objective != 0)
                ? ORC_E_ARG : build_graph(n, row_ptr, col_idx, T, M, &g, topo);
   if (st != ORC_OK) { r->status = st; goto done; }
 
@@ -439,9 +447,15 @@ oracle_result* oracle_solve(int n, const int32_t* row_ptr, const int32_t* col_id
         const int64_t* optL = r->opt + (size_t)(i * W);
         int64_t* optLp = r->opt + (size_t)(j * W);
         int32_t* argLp = r->arg + (size_t)(j * W);
+        int64_t least = INF;                /* min of opt[L, u] over u < t */
         for (int64_t t = 0; t <= TV; t++) {
           const int64_t m = optL[t];
           if (m == INF) continue;
+          /* the skip of Section 4.2 (last paragraph): an earlier t of the
+           * same row with strictly less memory makes this entry useless */
+          const int dominated = dominance_skip && least < m;
+          if (m < least) least = m;
+          if (dominated) continue;
           const int64_t Mcal = m + mem_terms;
           if (Mcal > B) continue;             /* memory constraint */
           const int64_t tp = t + dT;
@@ -516,6 +530,25 @@ done:
   free(g.T);
   free(g.M);
   return r;
+}
+
+oracle_result* oracle_solve(int n, const int32_t* row_ptr, const int32_t* col_idx,
+                            const int64_t* T, const int64_t* M, int mode, int64_t B,
+                            int objective, int64_t max_sets, int64_t max_sources) {
+  return solve_impl(n, row_ptr, col_idx, T, M, mode, B, objective, max_sets, max_sources, 0);
+}
+
+/*
+ * Algorithm 1 with the skip of Section 4.2's last paragraph: when t < t'
+ * and opt[L, t] < opt[L, t'], the entry opt[L, t'] is not propagated.  Any
+ * chain through (L, t') is matched by the same continuation from (L, t),
+ * faster and within the budget, so the time-centric t* and opt[V, t*] are
+ * unchanged while other entries may grow; only objective 0 is accepted.
+ */
+oracle_result* oracle_solve_dominance(int n, const int32_t* row_ptr, const int32_t* col_idx,
+                                      const int64_t* T, const int64_t* M, int mode, int64_t B,
+                                      int64_t max_sets) {
+  return solve_impl(n, row_ptr, col_idx, T, M, mode, B, 0, max_sets, -1, 1);
 }
 
 /* ---------------------------------------------------------- accessors */
