@@ -192,6 +192,34 @@ def dual_tables(rcdp, torch, reps=5, names=None):
     return out
 
 
+def dominance_fills(rcdp, torch, reps=5, names=None):
+    """rc_solve_dominance (the skip of Section 4.2 on the level fill) against
+    rc_solve on the same family: fill_ms of each (median of reps), and
+    `agrees` = equal (t*, opt[V, t*])."""
+    from paper_1905_11722_amd import workloads
+    out = {}
+    for name in names or ("resnet50", "unet", "densenet121"):
+        case = workloads.case(name)
+        g = rcdp.Graph.create(case.graph)
+        fam = g.build_family(case.mode)
+        dom, plain = [], []
+        for r in range(reps + 1):
+            a = fam.solve_dominance(case.B)
+            b = fam.solve(case.B, "tc")
+            if r > 0:
+                dom.append(a.fill_ms())
+                plain.append(b.fill_ms())
+            agrees = (a.t_star, a.m_star) == (b.t_star, b.m_star)
+            a.free()
+            b.free()
+        out[name] = {"fill_ms": round(sorted(dom)[len(dom) // 2], 4),
+                     "rc_solve_fill_ms": round(sorted(plain)[len(plain) // 2], 4),
+                     "agrees": agrees}
+        fam.free()
+        g.free()
+    return out
+
+
 def workloads_case(name):
     from paper_1905_11722_amd import workloads
     return workloads.case(name)
@@ -238,6 +266,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-other-graphs", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
+    ap.add_argument("--dominance", action="store_true",
+                    help="time only the level fill with the dominance skip (rc_solve_dominance) "
+                         "against rc_solve on --workload")
     ap.add_argument("--dual", action="store_true",
                     help="time only the memory-indexed table (rc_solve_dual) on --workload")
     args = ap.parse_args()
@@ -256,6 +287,10 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     rcdp.load_library()
+    if args.dominance:
+        res = dominance_fills(rcdp, torch, reps=max(3, args.steps), names=[args.workload])
+        print(json.dumps({"dominance": res}), flush=True)
+        return
     if args.dual:
         res = dual_tables(rcdp, torch, reps=max(3, args.steps), names=[args.workload])
         print(json.dumps({"dual": res}), flush=True)
@@ -289,6 +324,7 @@ def main():
 
     sweep = None if args.no_other_graphs else mc_sweep(rcdp, torch)
     dual = None if args.no_other_graphs else dual_tables(rcdp, torch)
+    dominance = None if args.no_other_graphs else dominance_fills(rcdp, torch, reps=3)
 
     out = {
         "metric": "DP cell relaxations/sec (whole step: family + fill + traceback)",
@@ -340,6 +376,7 @@ def main():
         "per_graph": per_graph,
         "mc_sweep": sweep,
         "dual": dual,
+        "dominance": dominance,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(case, W)

@@ -192,6 +192,23 @@ void rc_family_free(rc_family f);
 int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solution* out,
              int64_t* t_opt, int64_t* m_opt);
 /*
+ * rc_solve_dominance -- rc_solve (time-centric) with the skip of Section
+ * 4.2's last paragraph: a cell opt[L, t'] is not propagated when some t < t'
+ * of the same row has opt[L, t] < opt[L, t'].  The table is filled one size
+ * level at a time; once a level is done, each of its rows keeps only its
+ * weak front (the cells whose m is no larger than every earlier cell of the
+ * row) and stores every other cell as infinity, and later levels read no
+ * source cell past the end of that front.
+ *  t* and opt[V, t*] equal rc_solve's.  The exported table holds, at every
+ *  front cell, the value of Algorithm 1 run with the skip (it is the same
+ *  front as rc_solve's table), infinity elsewhere; the optarg of a front
+ *  cell and the schedule of rc_reconstruct follow Algorithm 1 with the skip
+ *  (the smallest family index among the sources that are propagated).
+ *  Other arguments, handles and errors as rc_solve.
+ */
+int rc_solve_dominance(rc_family f, int64_t B, void* stream, rc_solution* out, int64_t* t_opt,
+                       int64_t* m_opt);
+/*
  * rc_solve_batch -- rc_solve at nb budgets of one family in one pass: the
  * memory-centric sweep of Section 4.4 solves the same family at a range of
  * budgets.  The tables are filled together (for wide tables one launch of

@@ -23,6 +23,7 @@
 #include <algorithm>
 
 #include "rc_internal.h"
+#include "dominance.h"
 #include "schedule.h"
 
 namespace rcdp {
@@ -64,11 +65,14 @@ __global__ void k_solve_init(uint16_t* m, const int64_t* row_off, int objective,
 // other).  Block (x, y): cells [x * kTile, (x + 1) * kTile) of target
 // lb + y; each thread owns kCellsPerThread cells strided by the block size
 // so that every source read and every store of a wave is contiguous.
+// ws[i]: the source row's cells that may be read, t < ws[i] (its width w[i],
+// or the end of its weak front under the dominance skip).
 __global__ __launch_bounds__(kFillThreads) void k_fill_level(
     int64_t lb, const int32_t* __restrict__ w, const int64_t* __restrict__ row_off,
     const int64_t* __restrict__ pred_ptr, const int32_t* __restrict__ pidx,
     const int32_t* __restrict__ pdt, const int32_t* __restrict__ pdm,
-    const int32_t* __restrict__ pc, int32_t Beff, uint16_t* __restrict__ m) {
+    const int32_t* __restrict__ pc, int32_t Beff, const int32_t* __restrict__ ws,
+    uint16_t* __restrict__ m) {
   const int64_t j = lb + blockIdx.y;
   const int32_t wj = w[j];
   const int32_t tile0 = blockIdx.x * kTile;
@@ -83,7 +87,7 @@ __global__ __launch_bounds__(kFillThreads) void k_fill_level(
     if (tau < 0) continue;                    // no source cell can pass
     const int32_t dt = pdt[p];
     const int32_t i = pidx[p];
-    const int32_t wi = w[i];
+    const int32_t wi = ws[i];                 // cells of the source row that can be read
     if (dt >= tile0 + kTile || dt + wi <= tile0) continue;  // window misses the tile
     const uint16_t* src = m + row_off[i];
     const uint32_t dm = (uint32_t)pdm[p];
@@ -102,6 +106,89 @@ __global__ __launch_bounds__(kFillThreads) void k_fill_level(
     const int32_t tp = tile0 + r * kFillThreads + (int32_t)threadIdx.x;
     if (tp < wj) mo[tp] = (uint16_t)acc[r];
   }
+}
+
+// The dominance skip of Section 4.2 (last paragraph) on finished rows
+// lb + blockIdx.y: a cell t of row L is never propagated when an earlier
+// cell of the same row holds strictly less memory.  Such a cell is stored as
+// infinity, which leaves each row as its weak front (the cells with m no
+// larger than every earlier m), the only cells that a later level, the
+// selection of t* or the traceback reads.  we[L] = 1 + the last finite
+// cell kept (0 when none): the level fill reads no source cell beyond it.
+// Two passes over segments of kSeg cells, every (segment, row) a block:
+// k_front_min stores each segment's least m, then k_front takes the least m
+// of the segments before its own as the carry and scans its segment in
+// chunks of kFillThreads cells, each cell read and rewritten by one thread.
+constexpr int kSeg = 2048;
+
+__global__ __launch_bounds__(kFillThreads) void k_front_min(
+    int64_t lb, const int32_t* __restrict__ w, const int64_t* __restrict__ row_off,
+    const uint16_t* __restrict__ m, int32_t nseg, uint32_t* __restrict__ segmin,
+    int32_t* __restrict__ we) {
+  __shared__ uint32_t s_wave[kFillThreads / kWave];
+  const int64_t j = lb + blockIdx.y;
+  const int32_t wj = w[j];
+  const int32_t t0 = blockIdx.x * kSeg;
+  const uint16_t* row = m + row_off[j];
+  uint32_t x = kInfM;
+  for (int32_t t = t0 + (int32_t)threadIdx.x; t < min(wj, t0 + kSeg); t += kFillThreads)
+    x = min(x, (uint32_t)row[t]);
+  for (int off = kWave / 2; off > 0; off >>= 1) x = min(x, (uint32_t)__shfl_xor(x, off, kWave));
+  if (threadIdx.x % kWave == 0) s_wave[threadIdx.x / kWave] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int q = 1; q < kFillThreads / kWave; q++) x = min(x, s_wave[q]);
+    segmin[blockIdx.y * (int64_t)nseg + blockIdx.x] = x;
+    if (blockIdx.x == 0) we[j] = 0;
+  }
+}
+
+__global__ __launch_bounds__(kFillThreads) void k_front(
+    int64_t lb, const int32_t* __restrict__ w, const int64_t* __restrict__ row_off,
+    uint16_t* __restrict__ m, int32_t nseg, const uint32_t* __restrict__ segmin,
+    int32_t* __restrict__ we) {
+  __shared__ uint32_t s_wave[kFillThreads / kWave];
+  __shared__ int32_t s_last;
+  const int64_t j = lb + blockIdx.y;
+  const int32_t wj = w[j];
+  const int32_t s0 = blockIdx.x * kSeg;
+  if (s0 >= wj) return;                     // the whole block leaves together
+  const int32_t s1 = min(wj, s0 + kSeg);
+  uint16_t* row = m + row_off[j];
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  if (threadIdx.x == 0) s_last = -1;
+  uint32_t carry = kInfM;                   // least m of the earlier segments, then chunks
+  for (int32_t q = 0; q < (int32_t)blockIdx.x; q++)
+    carry = min(carry, segmin[blockIdx.y * (int64_t)nseg + q]);
+  int32_t last = -1;
+  for (int32_t c0 = s0; c0 < s1; c0 += kFillThreads) {
+    const int32_t t = c0 + (int32_t)threadIdx.x;
+    const uint32_t x = t < s1 ? row[t] : kInfM;
+    uint32_t inc = x;                       // inclusive minimum along the wave
+    for (int off = 1; off < kWave; off <<= 1) {
+      const uint32_t y = __shfl_up(inc, off, kWave);
+      if (lane >= off) inc = min(inc, y);
+    }
+    uint32_t exc = __shfl_up(inc, 1, kWave);
+    if (lane == 0) exc = kInfM;
+    if (lane == kWave - 1) s_wave[wave] = inc;
+    __syncthreads();
+    uint32_t before = carry;                // earlier chunks and earlier waves
+    for (int q = 0; q < wave; q++) before = min(before, s_wave[q]);
+    uint32_t chunk = carry;
+    for (int q = 0; q < kFillThreads / kWave; q++) chunk = min(chunk, s_wave[q]);
+    __syncthreads();                        // s_wave is rewritten by the next chunk
+    const uint32_t least = min(before, exc);
+    if (t < s1) {
+      const bool keep = x != kInfM && x <= least;
+      if (!keep && x != kInfM) row[t] = (uint16_t)kInfM;
+      if (keep) last = t;
+    }
+    carry = chunk;
+  }
+  if (last >= 0) atomicMax(&s_last, last);
+  __syncthreads();
+  if (threadIdx.x == 0 && s_last >= 0) atomicMax(&we[j], s_last + 1);
 }
 
 // optarg of every cell of targets [lb, lb + gridDim.y) from the final
@@ -301,7 +388,37 @@ hipError_t launch_fill(rc_solution sol, hipStream_t s) {
     if (tiles <= 0 || le <= lb) continue;
     hipLaunchKernelGGL(k_fill_level, dim3((unsigned)tiles, (unsigned)(le - lb)),
                        dim3(kFillThreads), 0, s, lb, f->w, f->row_off, f->pred_ptr, f->pidx,
-                       f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, sol->m);
+                       f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, f->w, sol->m);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_dominance(rc_solution sol, int32_t* we, hipStream_t s) {
+  rc_family f = sol->f;
+  const int64_t L = (int64_t)f->level_ptr.size() - 1;
+  int64_t most = 1;                         // segment minima of the largest level
+  for (int64_t l = 0; l < L; l++)
+    most = std::max<int64_t>(most, (f->level_ptr[l + 1] - f->level_ptr[l]) *
+                                       ((f->level_maxw[l] + kSeg - 1) / kSeg));
+  uint32_t* segmin = sol->arena.get_n<uint32_t>(most);
+  if (!segmin) return hipErrorOutOfMemory;
+  auto front = [&](int64_t lb, int64_t rows, int32_t maxw) {
+    const int32_t nseg = std::max<int32_t>(1, (maxw + kSeg - 1) / kSeg);
+    const dim3 grid((unsigned)nseg, (unsigned)rows);
+    hipLaunchKernelGGL(k_front_min, grid, dim3(kFillThreads), 0, s, lb, f->w, f->row_off,
+                       (const uint16_t*)sol->m, nseg, segmin, we);
+    hipLaunchKernelGGL(k_front, grid, dim3(kFillThreads), 0, s, lb, f->w, f->row_off, sol->m,
+                       nseg, (const uint32_t*)segmin, we);
+  };
+  front(0, 1, f->level_maxw[0]);            // the empty set
+  for (int64_t l = 1; l < L; l++) {
+    const int64_t lb = f->level_ptr[l], le = f->level_ptr[l + 1];
+    const int64_t tiles = (f->level_maxw[l] + kTile - 1) / kTile;
+    if (tiles <= 0 || le <= lb) continue;
+    hipLaunchKernelGGL(k_fill_level, dim3((unsigned)tiles, (unsigned)(le - lb)),
+                       dim3(kFillThreads), 0, s, lb, f->w, f->row_off, f->pred_ptr, f->pidx,
+                       f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, (const int32_t*)we, sol->m);
+    front(lb, le - lb, f->level_maxw[l]);
   }
   return hipGetLastError();
 }

@@ -11,6 +11,7 @@
 #include <vector>
 
 #include "rc_internal.h"
+#include "dominance.h"
 #include "dual.h"
 
 using namespace rcdp;
@@ -656,7 +657,8 @@ static int choose_fill_path(rc_family f) {
 }  // extern "C"
 
 // A solution handle with its buffers and events; nothing enqueued yet.
-static int new_solution(rc_family f, int64_t B, int32_t objective, rc_solution* out) {
+static int new_solution(rc_family f, int64_t B, int32_t objective, rc_solution* out,
+                        bool level_only = false) {
   if (!f || B < 0) return RC_E_ARG;
   if (objective != RC_TIME_CENTRIC && objective != RC_MEMORY_CENTRIC) return RC_E_ARG;
   const int64_t Beff = std::min<int64_t>(B, 2 * f->g->M_total);
@@ -685,7 +687,7 @@ static int new_solution(rc_family f, int64_t B, int32_t objective, rc_solution* 
     return fail(RC_E_NOMEM);
   if (hipEventCreate(&sol->ev0) != hipSuccess || hipEventCreate(&sol->ev1) != hipSuccess)
     return fail(RC_E_DEVICE);
-  sol->fill_path = choose_fill_path(f);
+  sol->fill_path = level_only ? 0 : choose_fill_path(f);
   if (sol->fill_path != 0 &&
       (hipEventCreate(&sol->evk0) != hipSuccess || hipEventCreate(&sol->evk1) != hipSuccess))
     return fail(RC_E_DEVICE);
@@ -741,12 +743,15 @@ static float elapsed(hipEvent_t a, hipEvent_t b) {
 
 extern "C" {
 
-int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solution* out,
-             int64_t* t_opt, int64_t* m_opt) {
+}  // extern "C"
+
+// rc_solve and rc_solve_dominance: one table fill, then the selection of t*.
+static int solve_one(rc_family f, int64_t B, int32_t objective, void* stream, rc_solution* out,
+                     int64_t* t_opt, int64_t* m_opt, bool dominance) {
   if (!f || !out) return RC_E_ARG;
   hipStream_t s = as_stream(stream);
   rc_solution sol = nullptr;
-  const int st0 = new_solution(f, B, objective, &sol);
+  const int st0 = new_solution(f, B, objective, &sol, dominance);
   if (st0 != RC_OK) return st0;
   auto fail = [&](int st) {
     (void)hipStreamSynchronize(s);
@@ -754,8 +759,11 @@ int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solutio
     return st;
   };
   if (launch_solve_init(sol, s) != hipSuccess) return fail(RC_E_DEVICE);
+  int32_t* we = nullptr;              // the skip: end of each row's weak front
+  if (dominance && !(we = sol->arena.get_n<int32_t>(f->F))) return fail(RC_E_NOMEM);
   if (hipEventRecord(sol->ev0, s) != hipSuccess) return fail(RC_E_DEVICE);
-  const hipError_t fe = sol->fill_path == 2   ? launch_fill_ghost(sol, s)
+  const hipError_t fe = dominance               ? launch_fill_dominance(sol, we, s)
+                        : sol->fill_path == 2   ? launch_fill_ghost(sol, s)
                         : sol->fill_path == 1 ? launch_fill_blocked(sol, s)
                                               : launch_fill(sol, s);
   if (fe != hipSuccess) {
@@ -779,6 +787,18 @@ int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solutio
   if (m_opt) *m_opt = sol->m_star;
   *out = sol;
   return st;
+}
+
+extern "C" {
+
+int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solution* out,
+             int64_t* t_opt, int64_t* m_opt) {
+  return solve_one(f, B, objective, stream, out, t_opt, m_opt, false);
+}
+
+int rc_solve_dominance(rc_family f, int64_t B, void* stream, rc_solution* out, int64_t* t_opt,
+                       int64_t* m_opt) {
+  return solve_one(f, B, RC_TIME_CENTRIC, stream, out, t_opt, m_opt, true);
 }
 
 int rc_solve_batch(rc_family f, const int64_t* B_host, int32_t nb, int32_t objective,

@@ -85,6 +85,8 @@ def load_library():
     lib.rc_family_free.argtypes = [P]
     lib.rc_solve.restype = ctypes.c_int
     lib.rc_solve.argtypes = [P, i64, i32, P, pp, ctypes.POINTER(i64), ctypes.POINTER(i64)]
+    lib.rc_solve_dominance.restype = ctypes.c_int
+    lib.rc_solve_dominance.argtypes = [P, i64, P, pp, ctypes.POINTER(i64), ctypes.POINTER(i64)]
     lib.rc_solution_fill_ms.restype = ctypes.c_int
     lib.rc_solution_fill_ms.argtypes = [P, ctypes.POINTER(ctypes.c_float)]
     lib.rc_solve_batch.restype = ctypes.c_int
@@ -305,6 +307,18 @@ class Family:
         st = lib.rc_solve(self._h, int(B), OBJECTIVES.get(objective, objective), _stream(),
                           ctypes.byref(h), ctypes.byref(t), ctypes.byref(m))
         _check(st, "rc_solve", allow=(OK, INFEASIBLE))
+        return Solution(h, self, st, t.value, m.value)
+
+    def solve_dominance(self, B):
+        """rc_solve_dominance: the time-centric solve with the dominance skip;
+        the table keeps each row's weak front, infinity elsewhere."""
+        lib = load_library()
+        h = ctypes.c_void_p()
+        t = ctypes.c_int64(-1)
+        m = ctypes.c_int64(-1)
+        st = lib.rc_solve_dominance(self._h, int(B), _stream(), ctypes.byref(h), ctypes.byref(t),
+                                    ctypes.byref(m))
+        _check(st, "rc_solve_dominance", allow=(OK, INFEASIBLE))
         return Solution(h, self, st, t.value, m.value)
 
     def free(self):
