@@ -81,6 +81,33 @@ def run_step(rcdp, g, case):
     return info, fill_ms, kernel_ms, t_star, sched
 
 
+def time_phases(rcdp, torch, case, steps):
+    """Per-phase host wall time of `steps` whole solves including the graph's
+    hand-over: rc_graph_create, rc_build_family, rc_solve, rc_reconstruct
+    (each returns after its results reached the host)."""
+    acc = {"graph_create_ms": [], "build_family_ms": [], "solve_ms": [], "reconstruct_ms": [],
+           "wall_ms": []}
+    for _ in range(steps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        g = rcdp.Graph.create(case.graph)
+        t1 = time.perf_counter()
+        fam = g.build_family(case.mode)
+        t2 = time.perf_counter()
+        sol = fam.solve(case.B, case.objective)
+        t3 = time.perf_counter()
+        if sol.feasible:
+            sol.reconstruct()
+        t4 = time.perf_counter()
+        for k, a, b in (("graph_create_ms", t0, t1), ("build_family_ms", t1, t2),
+                        ("solve_ms", t2, t3), ("reconstruct_ms", t3, t4), ("wall_ms", t0, t4)):
+            acc[k].append((b - a) * 1e3)
+        sol.free()
+        fam.free()
+        g.free()
+    return {k: round(sorted(v)[len(v) // 2], 4) for k, v in acc.items()}
+
+
 def time_case(rcdp, torch, case, steps, warmup):
     g = rcdp.Graph.create(case.graph)
     for _ in range(warmup):
@@ -95,7 +122,9 @@ def time_case(rcdp, torch, case, steps, warmup):
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     g.free()
+    phases = time_phases(rcdp, torch, case, steps)
     return {
+        "phases": phases,
         "ms_per_step": (t1 - t0) * 1e3 / steps,
         "fill_ms": sum(fills) / len(fills),
         "fill_ms_min": min(fills),
@@ -225,22 +254,96 @@ def workloads_case(name):
     return workloads.case(name)
 
 
+def host_description():
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count()
+    return {"nproc": usable, "cpu_count": os.cpu_count(), "cpu_model": model,
+            "omp_num_threads": os.environ.get("OMP_NUM_THREADS")}
+
+
 def cpu_baseline(case, relaxations):
+    """The oracle (Algorithm 1 as printed, t over 0..T(V)) on this host: one
+    full solve of the workload with the all-cores OpenMP build (the reported
+    value) and one with the single-threaded build, both rated against the
+    same relaxation count as the GPU.  Their tables are identical
+    (tests/test_oracle_parallel.py)."""
     from oracle import oracle
-    t0 = time.perf_counter()
-    r = oracle.solve(case.graph, case.mode, case.B, case.objective)
-    dt = time.perf_counter() - t0
+    legs = {}
+    for parallel in (True, False):
+        t0 = time.perf_counter()
+        r = oracle.solve(case.graph, case.mode, case.B, case.objective, parallel=parallel)
+        dt = time.perf_counter() - t0
+        legs[parallel] = (dt, r.t_star, r.num_sets, oracle.threads(parallel))
+        del r
+    dt, t_star, num_sets, cores = legs[True]
+    dt1, t_star1, _, _ = legs[False]
+    assert t_star1 == t_star
     return {
         "value": relaxations / dt,
         "unit": "relaxations/s",
-        "cores": 1,
+        "cores": cores,
         "kind": "oracle",
         "sample": (f"one full {case.objective.upper()} solve of {case.name} "
-                   f"(Algorithm 1 over all {r.num_sets} sets, t over 0..T(V)), "
-                   f"single thread, {dt:.1f} s; t*={r.t_star}"),
+                   f"(Algorithm 1 over all {num_sets} sets, t over 0..T(V)) with the "
+                   f"OpenMP build on {cores} threads, {dt:.2f} s; t*={t_star}"),
         "seconds": dt,
-        "t_star": r.t_star,
+        "t_star": t_star,
+        "one_core": {"value": relaxations / dt1, "seconds": dt1, "cores": 1},
+        "host": host_description(),
     }
+
+
+def measured_peaks(torch, copy_bytes=2 << 30):
+    """The chip's integer VALU rates and HBM copy bandwidth, measured now by
+    the microbenchmarks of libpeak.so (best of a few launches)."""
+    import ctypes
+
+    from paper_1905_11722_amd import build as hip_build
+    lib = ctypes.CDLL(hip_build.PEAK_LIB)
+    lib.peak_valu.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                              ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double)]
+    lib.peak_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                              ctypes.POINTER(ctypes.c_float)]
+    blocks = 256 * 16
+    out = torch.empty(blocks * 256, dtype=torch.int32, device="cuda")
+    res = {}
+    for kind, key in ((0, "valu_int32_tops"), (1, "valu_pk_u16_tops")):
+        best = 0.0
+        for rep in range(4):
+            ms, ops = ctypes.c_float(), ctypes.c_double()
+            assert lib.peak_valu(kind, blocks, 200, ctypes.c_void_p(out.data_ptr()),
+                                 ctypes.byref(ms), ctypes.byref(ops)) == 0
+            if rep:
+                best = max(best, ops.value / (ms.value / 1e3) / 1e12)
+        res[key] = best
+    src = torch.ones(copy_bytes // 4, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    best = 0.0
+    for rep in range(4):
+        ms = ctypes.c_float()
+        assert lib.peak_copy(ctypes.c_void_p(src.data_ptr()), ctypes.c_void_p(dst.data_ptr()),
+                             copy_bytes, 256 * 64, ctypes.byref(ms)) == 0
+        if rep:
+            best = max(best, 2 * copy_bytes / (ms.value / 1e3) / 1e9)
+    torch.cuda.synchronize()
+    assert bool((dst[-8:] == 1).all())
+    res["hbm_copy_gbs"] = best
+    res["copy_bytes"] = copy_bytes
+    res["note"] = ("independent add/min chains (32-bit and packed 16-bit), 4096 workgroups "
+                   "of 256; HBM: read + write bytes of a device-to-device copy")
+    del src, dst, out
+    return res
 
 
 def copy_calibration(nbytes):
@@ -313,7 +416,9 @@ def main():
             else:
                 r = time_case(rcdp, torch, workloads.case(name), max(3, args.steps // 4), 1)
             per_graph[name] = {
-                "wall_ms": round(r["ms_per_step"], 4),
+                "wall_ms": r["phases"]["wall_ms"],
+                "step_ms": round(r["ms_per_step"], 4),
+                "phases": r["phases"],
                 "fill_ms": round(r["fill_ms"], 4),
                 "relaxations": r["info"]["relaxations"],
                 "relax_per_s_fill": r["info"]["relaxations"] / (r["fill_ms"] / 1e3)
@@ -322,6 +427,7 @@ def main():
                 "k": r["k"],
             }
 
+    peaks = measured_peaks(torch)
     sweep = None if args.no_other_graphs else mc_sweep(rcdp, torch)
     dual = None if args.no_other_graphs else dual_tables(rcdp, torch)
     dominance = None if args.no_other_graphs else dominance_fills(rcdp, torch, reps=3)
@@ -354,6 +460,8 @@ def main():
             "relaxations": W,
             "t_star": main_res["t_star"],
         },
+        "phases": main_res["phases"],
+        "step_ms_with_graph_create": main_res["phases"]["wall_ms"],
         "fill_ms": main_res["fill_ms"],
         "fill_relax_per_s": W / fill_s,
         "fill_kernel_ms": {k: main_res[f"kernel_ms{s}"] for k, s in
@@ -372,7 +480,12 @@ def main():
             "kernel_ms": main_res["kernel_ms"],
             "ops_per_relaxation": OPS_PER_RELAXATION,
             "frac_of_int32_peak": achieved / VALU_INT32_PEAK_TOPS,
+            "measured_peak_pk_u16": peaks["valu_pk_u16_tops"],
+            "frac_of_measured_pk_u16": achieved / peaks["valu_pk_u16_tops"],
+            "measured_peak_int32": peaks["valu_int32_tops"],
+            "frac_of_measured_int32": achieved / peaks["valu_int32_tops"],
         },
+        "peaks": peaks,
         "per_graph": per_graph,
         "mc_sweep": sweep,
         "dual": dual,

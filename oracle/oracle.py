@@ -6,6 +6,7 @@ family, the whole opt / optarg table (rows on demand), t*, m* = opt[V, t*],
 the traced chain and its re-evaluated Eq. 1 overhead and Eq. 2 peak.
 """
 
+import contextlib
 import ctypes
 import os
 
@@ -18,17 +19,39 @@ E_ARG, E_CYCLE, E_COST, E_TOO_MANY_SETS, E_OVERFLOW, E_NOMEM, E_INTERNAL = -1, -
 MODES = {"exact": 0, "pruned": 1}
 OBJECTIVES = {"tc": 0, "mc": 1}
 
-_lib = None
+_libs = {}
 
 
-def _load():
-    global _lib
-    if _lib is not None:
-        return _lib
-    if not os.path.exists(_build.LIB):
+def _load(parallel=False):
+    """The single-threaded library, or (parallel=True) the OpenMP build of
+    the same source, whose results are identical."""
+    if parallel in _libs:
+        return _libs[parallel]
+    path = _build.LIB_OMP if parallel else _build.LIB
+    if not os.path.exists(path):
         _build.build()
-    _lib = open_library(_build.LIB)
-    return _lib
+    _libs[parallel] = open_library(path)
+    return _libs[parallel]
+
+
+@contextlib.contextmanager
+def using(lib):
+    """Run the single-threaded entry points on another compiled copy of the
+    oracle (a planted-mistake build in the tests) inside the block."""
+    saved = _libs.get(False)
+    _libs[False] = lib
+    try:
+        yield
+    finally:
+        if saved is None:
+            _libs.pop(False, None)
+        else:
+            _libs[False] = saved
+
+
+def threads(parallel=True):
+    """Threads the oracle's fill runs on in that build."""
+    return _load(parallel).oracle_threads()
 
 
 def open_library(path):
@@ -40,6 +63,9 @@ def open_library(path):
     lib.oracle_solve.restype = P
     lib.oracle_solve.argtypes = [ctypes.c_int, i32p, i32p, i64p, i64p, ctypes.c_int,
                                  ctypes.c_int64, ctypes.c_int, ctypes.c_int64, ctypes.c_int64]
+    lib.oracle_family.restype = P
+    lib.oracle_family.argtypes = [ctypes.c_int, i32p, i32p, i64p, i64p, ctypes.c_int,
+                                  ctypes.c_int64]
     lib.oracle_solve_dominance.restype = P
     lib.oracle_solve_dominance.argtypes = [ctypes.c_int, i32p, i32p, i64p, i64p, ctypes.c_int,
                                            ctypes.c_int64, ctypes.c_int64]
@@ -59,6 +85,8 @@ def open_library(path):
     lib.oracle_evaluate_chain.argtypes = [P, ctypes.c_int, i32p, i32p, i64p, i64p, i32p,
                                           ctypes.c_int, i64p, i64p, i64p]
     lib.oracle_free.argtypes = [P]
+    lib.oracle_threads.restype = ctypes.c_int
+    lib.oracle_threads.argtypes = []
     return lib
 
 
@@ -76,8 +104,8 @@ def _ptr(a, ctype):
 class OracleResult:
     """Result of one oracle run; frees the C result when collected."""
 
-    def __init__(self, graph, handle):
-        self._lib = _load()
+    def __init__(self, graph, handle, lib):
+        self._lib = lib
         self._h = handle
         self.graph = graph
         L = self._lib
@@ -153,10 +181,11 @@ class OracleResult:
 
 
 def solve(graph, mode, B, objective="tc", max_sets=1 << 20, max_sources=-1, csr=None,
-          T=None, M=None):
+          T=None, M=None, parallel=False):
     """Run the oracle.  ``graph`` is a workloads.Graph; ``csr``/``T``/``M``
-    override its arrays (used to feed invalid inputs)."""
-    lib = _load()
+    override its arrays (used to feed invalid inputs).  ``parallel`` runs the
+    OpenMP build (same results, all cores)."""
+    lib = _load(parallel)
     row_ptr, col_idx = csr if csr is not None else graph.csr()
     T = graph.T if T is None else T
     M = graph.M if M is None else M
@@ -169,14 +198,29 @@ def solve(graph, mode, B, objective="tc", max_sets=1 << 20, max_sources=-1, csr=
                          int(max_sets), int(max_sources))
     if not h:
         raise MemoryError("oracle_solve returned NULL")
-    return OracleResult(graph, h)
+    return OracleResult(graph, h, lib)
 
 
-def solve_dominance(graph, mode, B, max_sets=1 << 20):
+def family(graph, mode, max_sets=1 << 20):
+    """The lower-set family of Algorithm 1 only (no table): a result whose
+    sets() and T_total are valid, in the family order of the solve."""
+    lib = _load()
+    row_ptr, col_idx = graph.csr()
+    rp, ci = _arr(row_ptr, np.int32), _arr(col_idx, np.int32)
+    Ta, Ma = _arr(graph.T, np.int64), _arr(graph.M, np.int64)
+    h = lib.oracle_family(graph.n, _ptr(rp, ctypes.c_int32), _ptr(ci, ctypes.c_int32),
+                          _ptr(Ta, ctypes.c_int64), _ptr(Ma, ctypes.c_int64),
+                          MODES[mode] if isinstance(mode, str) else mode, int(max_sets))
+    if not h:
+        raise MemoryError("oracle_family returned NULL")
+    return OracleResult(graph, h, lib)
+
+
+def solve_dominance(graph, mode, B, max_sets=1 << 20, parallel=False):
     """Algorithm 1 with the dominance skip of Section 4.2's last paragraph
     (time-centric only): the same t* and opt[V, t*], a table whose entries
     are never below solve()'s."""
-    lib = _load()
+    lib = _load(parallel)
     row_ptr, col_idx = graph.csr()
     rp, ci = _arr(row_ptr, np.int32), _arr(col_idx, np.int32)
     Ta, Ma = _arr(graph.T, np.int64), _arr(graph.M, np.int64)
@@ -186,10 +230,10 @@ def solve_dominance(graph, mode, B, max_sets=1 << 20):
                                    int(max_sets))
     if not h:
         raise MemoryError("oracle_solve_dominance returned NULL")
-    return OracleResult(graph, h)
+    return OracleResult(graph, h, lib)
 
 
-def min_budget(graph, mode):
+def min_budget(graph, mode, parallel=False):
     """The smallest budget B for which the family admits a strategy.
 
     Section 5 runs its experiments at this budget and finds it by binary
@@ -201,7 +245,7 @@ def min_budget(graph, mode):
     lo, hi = -1, 2 * int(sum(graph.M))
     while hi - lo > 1:
         mid = (lo + hi) // 2
-        if solve(graph, mode, mid, "tc").status == OK:
+        if solve(graph, mode, mid, "tc", parallel=parallel).status == OK:
             hi = mid
         else:
             lo = mid

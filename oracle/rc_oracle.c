@@ -10,7 +10,10 @@
  * Section 4.4.
  *
  * Only the tests, the smoke check and the benchmark's CPU-baseline leg may
- * load this code.  It shares nothing with the GPU library: sets are plain
+ * load this code.  The same source builds a single-threaded library and,
+ * with OpenMP, an all-cores one whose tables are identical (the targets of
+ * one source are split among threads; sources stay in order).  It shares
+ * nothing with the GPU library: sets are plain
  * 0/1 byte arrays over the node ids, every set expression of Algorithm 1 is
  * formed explicitly for every (L, L') pair, and t runs over the whole range
  * 0..T(V) as printed.  Nothing is blocked, fused or reordered.
@@ -46,6 +49,9 @@
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 #define ORC_OK 0
 #define ORC_INFEASIBLE 1
@@ -328,7 +334,7 @@ void oracle_free(oracle_result* r);
 static oracle_result* solve_impl(int n, const int32_t* row_ptr, const int32_t* col_idx,
                                  const int64_t* T, const int64_t* M, int mode, int64_t B,
                                  int objective, int64_t max_sets, int64_t max_sources,
-                                 int dominance_skip) {
+                                 int dominance_skip, int family_only) {
   oracle_result* r = (oracle_result*)calloc(1, sizeof(oracle_result));
   if (!r) return NULL;
   r->n = n;
@@ -382,6 +388,11 @@ static oracle_result* solve_impl(int n, const int32_t* row_ptr, const int32_t* c
     r->sets = f.sets;
     r->num_sets = f.count;
   }
+  if (family_only) {
+    for (int v = 0; v < n; v++) r->T_total += g.T[v];
+    r->status = ORC_OK;
+    goto done;
+  }
 
   {
     const int64_t F = r->num_sets;
@@ -409,10 +420,7 @@ static oracle_result* solve_impl(int n, const int32_t* row_ptr, const int32_t* c
     u8* dmdp = (u8*)calloc((size_t)n + 1, 1);
     u8* dmo = (u8*)calloc((size_t)n + 1, 1);
     u8* tmp = (u8*)calloc((size_t)2 * n + 2, 1);
-    u8* Vp = (u8*)calloc((size_t)n + 1, 1);
-    u8* Vpb = (u8*)calloc((size_t)n + 1, 1);
-    u8* bdl = (u8*)calloc((size_t)n + 1, 1);
-    if (!bdall || !outm) { st = ORC_E_NOMEM; goto fail_loop; }
+    if (!bdall || !outm || !dp || !dpo || !dmdp || !dmo || !tmp) { st = ORC_E_NOMEM; goto fail_loop; }
     for (int64_t j = 0; j < F; j++) {
       const u8* Lp = r->sets + (size_t)j * n;
       delta_plus(&g, Lp, dp);
@@ -423,54 +431,81 @@ static oracle_result* solve_impl(int n, const int32_t* row_ptr, const int32_t* c
       boundary(&g, Lp, bdall + (size_t)j * n, tmp);
     }
 
-    int64_t sources = max_sources < 0 ? F : (max_sources < F ? max_sources : F);
-    /* for L in the family in ascending order of size */
-    for (int64_t i = 0; i < sources; i++) {
-      const u8* L = r->sets + (size_t)i * n;
-      /* for L' in the family with L a proper subset of L' */
-      for (int64_t j = 0; j < F; j++) {
-        const u8* Lp = r->sets + (size_t)j * n;
-        if (!proper_subset(n, L, Lp)) continue;
-        r->num_pairs++;
-        r->relaxations_literal += TV + 1;
-        const u8* bd = bdall + (size_t)j * n;
-        /* V' = L' \ L */
-        set_minus(n, Lp, L, Vp);
-        /* 2 M(V') + M(delta+(L') \ L') + M(delta-(delta+(L')) \ L') */
-        const int64_t mem_terms = 2 * cost_sum(n, Vp, g.M) + outm[j];
-        /* T(V' \ boundary(L')) and M(boundary(L') \ L) */
-        set_minus(n, Vp, bd, Vpb);
-        const int64_t dT = cost_sum(n, Vpb, g.T);
-        set_minus(n, bd, L, bdl);
-        const int64_t dM = cost_sum(n, bdl, g.M);
-        /* for t = 0..T(V) */
-        const int64_t* optL = r->opt + (size_t)(i * W);
-        int64_t* optLp = r->opt + (size_t)(j * W);
-        int32_t* argLp = r->arg + (size_t)(j * W);
-        int64_t least = INF;                /* min of opt[L, u] over u < t */
-        for (int64_t t = 0; t <= TV; t++) {
-          const int64_t m = optL[t];
-          if (m == INF) continue;
-          /* the skip of Section 4.2 (last paragraph): an earlier t of the
-           * same row with strictly less memory makes this entry useless */
-          const int dominated = dominance_skip && least < m;
-          if (m < least) least = m;
-          if (dominated) continue;
-          const int64_t Mcal = m + mem_terms;
-          if (Mcal > B) continue;             /* memory constraint */
-          const int64_t tp = t + dT;
-          const int64_t mp = m + dM;
-          if (tp > TV) { st = ORC_E_INTERNAL; goto fail_loop; }
-          if (optLp[tp] > mp) {               /* update DP array */
-            optLp[tp] = mp;
-            argLp[tp] = (int32_t)i;
+    const int64_t sources = max_sources < 0 ? F : (max_sources < F ? max_sources : F);
+    int64_t pairs = 0, literal = 0;
+    int err = ORC_OK;
+    /* Built with OpenMP (the all-cores timing build), the targets L' of one
+     * source L are shared among threads: each thread owns whole rows L',
+     * and L still advances in family order, so every cell sees its updates
+     * in the order of the sequential loop and ends with the same value and
+     * optarg.  Built without it, the pragmas are ignored. */
+#pragma omp parallel reduction(+ : pairs, literal)
+    {
+      u8* Vp = (u8*)calloc((size_t)n + 1, 1);
+      u8* Vpb = (u8*)calloc((size_t)n + 1, 1);
+      u8* bdl = (u8*)calloc((size_t)n + 1, 1);
+      if (!Vp || !Vpb || !bdl) {
+#pragma omp atomic write
+        err = ORC_E_NOMEM;
+      }
+      /* for L in the family in ascending order of size */
+      for (int64_t i = 0; i < sources; i++) {
+        const u8* L = r->sets + (size_t)i * n;
+        /* for L' in the family with L a proper subset of L' */
+#pragma omp for schedule(dynamic, 4)
+        for (int64_t j = 0; j < F; j++) {
+          if (!Vp || !Vpb || !bdl) continue;
+          const u8* Lp = r->sets + (size_t)j * n;
+          if (!proper_subset(n, L, Lp)) continue;
+          pairs++;
+          literal += TV + 1;
+          const u8* bd = bdall + (size_t)j * n;
+          /* V' = L' \ L */
+          set_minus(n, Lp, L, Vp);
+          /* 2 M(V') + M(delta+(L') \ L') + M(delta-(delta+(L')) \ L') */
+          const int64_t mem_terms = 2 * cost_sum(n, Vp, g.M) + outm[j];
+          /* T(V' \ boundary(L')) and M(boundary(L') \ L) */
+          set_minus(n, Vp, bd, Vpb);
+          const int64_t dT = cost_sum(n, Vpb, g.T);
+          set_minus(n, bd, L, bdl);
+          const int64_t dM = cost_sum(n, bdl, g.M);
+          /* for t = 0..T(V) */
+          const int64_t* optL = r->opt + (size_t)(i * W);
+          int64_t* optLp = r->opt + (size_t)(j * W);
+          int32_t* argLp = r->arg + (size_t)(j * W);
+          int64_t least = INF;                /* min of opt[L, u] over u < t */
+          for (int64_t t = 0; t <= TV; t++) {
+            const int64_t m = optL[t];
+            if (m == INF) continue;
+            /* the skip of Section 4.2 (last paragraph): an earlier t of the
+             * same row with strictly less memory makes this entry useless */
+            const int dominated = dominance_skip && least < m;
+            if (m < least) least = m;
+            if (dominated) continue;
+            const int64_t Mcal = m + mem_terms;
+            if (Mcal > B) continue;             /* memory constraint */
+            const int64_t tp = t + dT;
+            const int64_t mp = m + dM;
+            if (tp > TV) {
+#pragma omp atomic write
+              err = ORC_E_INTERNAL;
+              break;
+            }
+            if (optLp[tp] > mp) {               /* update DP array */
+              optLp[tp] = mp;
+              argLp[tp] = (int32_t)i;
+            }
           }
         }
       }
+      free(Vp); free(Vpb); free(bdl);
     }
+    r->num_pairs = pairs;
+    r->relaxations_literal = literal;
+    if (err != ORC_OK) st = err;
   fail_loop:
-    free(Vp); free(dp); free(dpo); free(dmdp); free(dmo); free(Vpb);
-    free(bdl); free(tmp); free(bdall); free(outm);
+    free(dp); free(dpo); free(dmdp); free(dmo);
+    free(tmp); free(bdall); free(outm);
     if (st != ORC_OK) goto fail;
     if (max_sources >= 0) { r->status = ORC_OK; goto done; }
 
@@ -535,7 +570,14 @@ done:
 oracle_result* oracle_solve(int n, const int32_t* row_ptr, const int32_t* col_idx,
                             const int64_t* T, const int64_t* M, int mode, int64_t B,
                             int objective, int64_t max_sets, int64_t max_sources) {
-  return solve_impl(n, row_ptr, col_idx, T, M, mode, B, objective, max_sets, max_sources, 0);
+  return solve_impl(n, row_ptr, col_idx, T, M, mode, B, objective, max_sets, max_sources, 0, 0);
+}
+
+/* The family of Algorithm 1 alone (mode as oracle_solve), in its order, with
+ * no table: oracle_get_sets and oracle_T_total are valid on the result. */
+oracle_result* oracle_family(int n, const int32_t* row_ptr, const int32_t* col_idx,
+                             const int64_t* T, const int64_t* M, int mode, int64_t max_sets) {
+  return solve_impl(n, row_ptr, col_idx, T, M, mode, 0, 0, max_sets, -1, 0, 1);
 }
 
 /*
@@ -548,10 +590,19 @@ oracle_result* oracle_solve(int n, const int32_t* row_ptr, const int32_t* col_id
 oracle_result* oracle_solve_dominance(int n, const int32_t* row_ptr, const int32_t* col_idx,
                                       const int64_t* T, const int64_t* M, int mode, int64_t B,
                                       int64_t max_sets) {
-  return solve_impl(n, row_ptr, col_idx, T, M, mode, B, 0, max_sets, -1, 1);
+  return solve_impl(n, row_ptr, col_idx, T, M, mode, B, 0, max_sets, -1, 1, 0);
 }
 
 /* ---------------------------------------------------------- accessors */
+
+/* Threads the fill loop runs on: 1 unless built with OpenMP. */
+int oracle_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
 
 int oracle_status(const oracle_result* r) { return r->status; }
 int64_t oracle_num_sets(const oracle_result* r) { return r->num_sets; }

@@ -6,9 +6,9 @@ its weak front only (the cells no earlier cell of the row beats on memory)
 and stores infinity elsewhere, so its table must equal the oracle's skipped
 table with that same front taken row by row, bit for bit; the optarg of every
 front cell, t*, opt[V, t*] and the traced schedule (same tie rule) must equal
-the oracle's.  At the full size of the 121-layer DenseNet, where the oracle is
-too slow, t* and opt[V, t*] are checked against rc_solve and sampled rows
-against the front of rc_solve's row (the skip keeps every row's front).
+the oracle's.  The full-size ResNet-50, DenseNet-121 and U-Net shapes run the
+same comparison against the oracle's all-cores build (identical results,
+pinned in test_oracle_parallel.py).
 """
 
 import numpy as np
@@ -40,9 +40,9 @@ def front(rows):
     return np.where(keep, rows, -1), keep
 
 
-def compare(rc, g, mode, B):
+def compare(rc, g, mode, B, parallel=False):
     fam = rc.Graph.create(g).build_family(mode)
-    ref = O.solve_dominance(g, mode, B)
+    ref = O.solve_dominance(g, mode, B, parallel=parallel)
     assert ref.status in (O.OK, O.INFEASIBLE)
     sol = fam.solve_dominance(B)
     full = fam.solve(B, "tc")
@@ -107,15 +107,10 @@ def test_degenerate(rc):
         rc.Graph.create(g1).build_family("exact").solve_dominance(-1)
 
 
-def test_densenet121_full_size(rc):
-    c = W.case("densenet121")
-    fam = rc.Graph.create(c.graph).build_family(c.mode)
-    sol = fam.solve_dominance(c.B)
-    full = fam.solve(c.B, "tc")
-    assert (sol.t_star, sol.m_star) == (full.t_star, full.m_star)
-    sched = sol.reconstruct()
-    assert (sched.overhead, sched.cache_mem) == (sol.t_star, sol.m_star) and sched.peak <= c.B
-    F = fam.info["num_sets"]
-    for first in (0, F // 3, F // 2, F - 16):
-        m, _ = sol.table(first, 16)
-        np.testing.assert_array_equal(front(full.table(first, 16)[0])[0], m)
+@pytest.mark.slow
+@pytest.mark.parametrize("name", ["resnet50", "unet", "densenet121"])
+def test_full_size_against_oracle(rc, name):
+    """The whole skipped table (every row's front), the optarg of every front
+    cell, t*, opt[V, t*] and the schedule against the oracle with the skip."""
+    c = W.case(name)
+    compare(rc, c.graph, c.mode, c.B, parallel=True)

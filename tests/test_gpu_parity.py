@@ -26,12 +26,12 @@ def rc():
     return rcdp
 
 
-def compare(rc, O, g, mode, B, objectives=("tc", "mc"), table=True):
+def compare(rc, O, g, mode, B, objectives=("tc", "mc"), table=True, parallel=False):
     gg = rc.Graph.create(g)
     fam = gg.build_family(mode)
     ref = None
     for objective in objectives:
-        ref = O.solve(g, mode, B, objective)
+        ref = O.solve(g, mode, B, objective, parallel=parallel)
         assert ref.status in (O.OK, O.INFEASIBLE), ref.status
         sol = fam.solve(B, objective)
         assert fam.info["num_sets"] == ref.num_sets
@@ -179,7 +179,7 @@ def test_repeatable(rc, oracle_mod):
 def test_full_size_cases(rc, oracle_mod, name):
     """The CNN-shaped cases at full size, whole table."""
     c = W.case(name)
-    compare(rc, oracle_mod, c.graph, c.mode, c.B)
+    compare(rc, oracle_mod, c.graph, c.mode, c.B, parallel=True)
 
 
 # ---------------------------------------------------------------- fill paths
@@ -324,29 +324,41 @@ def mc_budgets(b_min, m_total, count=32):
     return [b_min + (j * (top - b_min)) // (count - 1) for j in range(count)]
 
 
+@pytest.mark.slow
 def test_mc_sweep_resnet50(rc, oracle_mod):
     """The memory-centric sweep of the ResNet-50-shaped graph over 32 budgets
-    (Section 4.4): t_MC never decreases with the budget, every traced schedule
-    re-evaluates to its own t and stays within its budget, the sweep ends at
-    t_MC = T(V) at B = 2 M(V), and sampled budgets match the oracle."""
+    (Section 4.4) in one batched fill: at every budget t_MC, opt[V, t_MC],
+    the traced chain, seg, cached and the Eq. 1 / Eq. 2 re-evaluation equal
+    the oracle's; the whole table equals the oracle's at the smallest
+    budget, two interior ones and 2 M(V); t_MC never decreases with the
+    budget and reaches T(V) at 2 M(V)."""
     c = W.case("resnet50")
     g = c.graph
     fam = rc.Graph.create(g).build_family("pruned")
     b_min = fam.min_budget()
+    assert b_min == oracle_mod.min_budget(g, "pruned", parallel=True)
     budgets = mc_budgets(b_min, sum(g.M))
     prev = -1
     for j, (B, sol) in enumerate(fam.sweep(budgets, "mc")):
-        assert sol.feasible
+        ref = oracle_mod.solve(g, "pruned", B, "mc", parallel=True)
+        assert ref.status == oracle_mod.OK and sol.feasible, j
+        assert (sol.t_star, sol.m_star) == (ref.t_star, ref.m_star), j
         sched = sol.reconstruct()
-        assert sched.overhead == sol.t_star
-        assert sched.peak <= B
-        assert sol.t_star >= prev
+        chain, seg, cached = ref.schedule()
+        np.testing.assert_array_equal(sched.chain, chain, err_msg=f"budget {j}")
+        np.testing.assert_array_equal(sched.seg, seg)
+        np.testing.assert_array_equal(sched.cached, cached)
+        assert (sched.overhead, sched.peak, sched.cache_mem) == (
+            ref.overhead, ref.peak, ref.cache_mem), j
+        assert sched.peak <= B and sol.t_star >= prev
         prev = sol.t_star
-        if j in (0, 11, 31):
-            ref = oracle_mod.solve(g, "pruned", B, "mc")
-            assert (sol.t_star, sol.m_star) == (ref.t_star, ref.m_star)
-            chain, _, _ = ref.schedule()
-            np.testing.assert_array_equal(sched.chain, chain)
+        if j in (0, 10, 21, 31):
+            m, a = sol.table()
+            rm, ra = ref.table()
+            np.testing.assert_array_equal(m, rm, err_msg=f"budget {j}")
+            np.testing.assert_array_equal(a, ra, err_msg=f"budget {j}")
+            del m, a, rm, ra
+        del ref
         sol.free()
     assert prev == sum(g.T)
 

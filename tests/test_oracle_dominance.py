@@ -106,10 +106,7 @@ def _budgets(g):
 def exact_pins_hold(lib=None):
     """The exact closed form and t*, m* on the tiny graphs; False on the first
     failure.  lib: a mutant library to run instead of the oracle's."""
-    saved = O._lib
-    if lib is not None:
-        O._lib = lib
-    try:
+    with O.using(lib if lib is not None else O._load()):
         for g in TINY:
             for B in _budgets(g):
                 for mode in ("exact", "pruned"):
@@ -127,8 +124,6 @@ def exact_pins_hold(lib=None):
                     if (r.t_star, r.m_star) != (ts, bopt[(len(F) - 1, ts)]):
                         return False
         return True
-    finally:
-        O._lib = saved
 
 
 def test_exact_closed_form_on_tiny_graphs():

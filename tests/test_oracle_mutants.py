@@ -44,9 +44,7 @@ MUTANTS = {
 
 def quick_pins_hold(lib):
     """A fast subset of the pins; False as soon as one fails."""
-    saved = O._lib
-    O._lib = lib
-    try:
+    with O.using(lib):
         graphs = [W.random_dag(n, p, s, tmax=9, mmax=7)
                   for n, p, s in [(5, 0.3, 1), (6, 0.5, 2), (6, 0.2, 3), (7, 0.4, 4), (4, 0.6, 5)]]
         graphs.append(W.ladder(3, seed=2, tmax=9, mmax=9))
@@ -93,8 +91,7 @@ def quick_pins_hold(lib):
                 if r.evaluate_chain(chain) != bf.evaluate_chain(bf.SetGraph(g), [F[c] for c in chain]):
                     return False
         return True
-    finally:
-        O._lib = saved
+
 
 
 def test_unmutated_oracle_passes():
