@@ -37,6 +37,75 @@ void set_last_error_msg(const char* msg) {
   std::snprintf(g_last_error, sizeof(g_last_error), "%s", msg);
 }
 
+// Sizes of the memory-indexed table of one solve (rc_solve_dual): argument
+// checks, the effective budget, the row width and the scratch it needs.
+int dual_buffers(rc_family f, int64_t B, int32_t objective, DualBuffers* out) {
+  if (!f || B < 0) return RC_E_ARG;
+  if (objective != RC_TIME_CENTRIC && objective != RC_MEMORY_CENTRIC) return RC_E_ARG;
+  const int64_t Beff = std::min<int64_t>(B, 2 * f->g->M_total);
+  const int64_t W = std::min<int64_t>(Beff, f->g->M_total) + 1;
+  if (f->g->T_total >= (int64_t)UINT32_MAX || W > INT32_MAX / 2 ||
+      (double)f->F * (double)W > (double)((int64_t)1 << 31))
+    return RC_E_OVERFLOW;
+  *out = DualBuffers();
+  out->Beff = Beff;
+  out->W = W;
+  out->cells = f->F * W;
+  return RC_OK;
+}
+
+// The memory-indexed table, its selection and (when any schedule output is
+// asked for) its traceback, in the device buffers of b; results to the host
+// outputs.  Synchronises s.  e0 / e1 (may be null) bracket the table's
+// kernels.  Allocates nothing.
+int dual_solve(rc_family f, int32_t objective, const DualBuffers& b, hipEvent_t e0,
+               hipEvent_t e1, hipStream_t s, int64_t* t_opt, int64_t* m_opt, int32_t* k,
+               int32_t* chain_host, int32_t* seg_host, uint8_t* cached_host, int64_t* overhead,
+               int64_t* peak, int64_t* cache_mem) {
+  const hipError_t le = launch_dual(f, f->level_pairs, (int32_t)b.Beff, (int32_t)b.W, objective,
+                                    b.D, b.st, e0, e1, s);
+  if (le != hipSuccess) {
+    set_last_error("dual table launch", le);
+    return RC_E_DEVICE;
+  }
+  DevStatus hs;
+  RC_HIP(hipMemcpyAsync(&hs, b.st, sizeof(hs), hipMemcpyDeviceToHost, s));
+  RC_HIP(hipStreamSynchronize(s));
+  const bool schedule = k || chain_host || seg_host || cached_host || overhead || peak || cache_mem;
+  if (schedule && hs.t_sel >= 0) {
+    const int n = f->g->n;
+    const hipError_t te = launch_dual_trace(f, (int32_t)b.Beff, (int32_t)b.W, objective, b.D,
+                                            b.st, b.chain, b.seg, b.cached, s);
+    if (te != hipSuccess) {
+      set_last_error("dual traceback launch", te);
+      return RC_E_DEVICE;
+    }
+    DevStatus ts;
+    RC_HIP(hipMemcpyAsync(&ts, b.st, sizeof(ts), hipMemcpyDeviceToHost, s));
+    RC_HIP(hipStreamSynchronize(s));
+    if (ts.error || ts.k < 0 || ts.k > f->F) {
+      set_last_error_msg("dual traceback: the walk did not end at (empty set, 0, 0)");
+      return RC_E_DEVICE;
+    }
+    if (chain_host && ts.k > 0)
+      RC_HIP(hipMemcpyAsync(chain_host, b.chain, sizeof(int32_t) * (size_t)ts.k,
+                            hipMemcpyDeviceToHost, s));
+    if (seg_host && n > 0)
+      RC_HIP(hipMemcpyAsync(seg_host, b.seg, sizeof(int32_t) * (size_t)n, hipMemcpyDeviceToHost,
+                            s));
+    if (cached_host && n > 0)
+      RC_HIP(hipMemcpyAsync(cached_host, b.cached, (size_t)n, hipMemcpyDeviceToHost, s));
+    RC_HIP(hipStreamSynchronize(s));
+    if (k) *k = ts.k;
+    if (overhead) *overhead = ts.overhead;
+    if (peak) *peak = ts.peak;
+    if (cache_mem) *cache_mem = ts.cache_mem;
+  }
+  if (t_opt) *t_opt = hs.t_sel;
+  if (m_opt) *m_opt = hs.t_sel >= 0 ? hs.m_sel : -1;
+  return hs.t_sel >= 0 ? RC_OK : RC_INFEASIBLE;
+}
+
 void* Arena::raw(size_t bytes) {
   void* p = nullptr;
   if (alloc) {
@@ -391,6 +460,9 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
   RC_HIP(hipMemcpyAsync(f->w_host.data(), f->w, sizeof(int32_t) * F, hipMemcpyDeviceToHost, s));
   RC_HIP(hipMemcpyAsync(f->row_off_host.data(), f->row_off, sizeof(int64_t) * (F + 1),
                         hipMemcpyDeviceToHost, s));
+  std::vector<int64_t> pred_ptr_h(F + 1);
+  RC_HIP(hipMemcpyAsync(pred_ptr_h.data(), f->pred_ptr, sizeof(int64_t) * (F + 1),
+                        hipMemcpyDeviceToHost, s));
   RC_HIP(hipMemcpyAsync(&hs, f->status, sizeof(hs), hipMemcpyDeviceToHost, s));
   f->rec_total = 0;
   if (f->nblk > 0)
@@ -415,6 +487,15 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
     f->max_row = std::max<int64_t>(f->max_row, f->w_host[i]);
   }
   f->level_ptr.push_back(F);
+  // the most pairs of a target per size level (the memory-indexed table
+  // runs that many pairs per level launch)
+  f->level_pairs.clear();
+  for (size_t l = 0; l + 1 < f->level_ptr.size(); l++) {
+    int64_t most = 0;
+    for (int64_t j = f->level_ptr[l]; j < f->level_ptr[l + 1]; j++)
+      most = std::max(most, pred_ptr_h[j + 1] - pred_ptr_h[j]);
+    f->level_pairs.push_back(most);
+  }
   if (near_d) {                                // kind not fixed before the host copies
     if (f->blk_kind < 0) f->blk_kind = family_block_kind(f, true);
     cut_blocks(f, near_h);
@@ -514,13 +595,9 @@ int rc_solve_dual(rc_family f, int64_t B, int32_t objective, void* stream, int64
                   int64_t* m_opt, float* fill_ms, int32_t* k, int32_t* chain_host,
                   int32_t* seg_host, uint8_t* cached_host, int64_t* overhead, int64_t* peak,
                   int64_t* cache_mem) {
-  if (!f || B < 0) return RC_E_ARG;
-  if (objective != RC_TIME_CENTRIC && objective != RC_MEMORY_CENTRIC) return RC_E_ARG;
-  const int64_t Beff = std::min<int64_t>(B, 2 * f->g->M_total);
-  const int64_t W = std::min<int64_t>(Beff, f->g->M_total) + 1;
-  if (f->g->T_total >= (int64_t)UINT32_MAX || W > INT32_MAX / 2 ||
-      (double)f->F * (double)W > (double)((int64_t)1 << 31))
-    return RC_E_OVERFLOW;
+  DualBuffers need;
+  const int st0 = dual_buffers(f, B, objective, &need);
+  if (st0 != RC_OK) return st0;
   hipStream_t s = as_stream(stream);
   rcdp::Arena A;
   A.alloc = f->arena.alloc;
@@ -534,78 +611,23 @@ int rc_solve_dual(rc_family f, int64_t B, int32_t objective, void* stream, int64
     A.release_all();
     return st;
   };
-  uint32_t* D = A.get_n<uint32_t>(f->F * W);
-  DevStatus* dst = A.get_n<DevStatus>(1);
-  if (!D || !dst) return finish(RC_E_NOMEM);
+  DualBuffers buf = need;
+  buf.D = A.get_n<uint32_t>(need.cells);
+  buf.st = A.get_n<DevStatus>(1);
+  buf.chain = A.get_n<int32_t>(f->F);
+  buf.seg = A.get_n<int32_t>(f->g->n);
+  buf.cached = A.get_n<uint8_t>(f->g->n);
+  if (!buf.D || !buf.st || !buf.chain || !buf.seg || !buf.cached) return finish(RC_E_NOMEM);
   if (fill_ms && (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess))
     return finish(RC_E_DEVICE);
-  // the most pairs of a target per size level: the pair runs of each launch
-  std::vector<int64_t> pp(f->F + 1), level_pairs;
-  if (hipMemcpyAsync(pp.data(), f->pred_ptr, sizeof(int64_t) * pp.size(), hipMemcpyDeviceToHost,
-                     s) != hipSuccess ||
-      hipStreamSynchronize(s) != hipSuccess)
-    return finish(RC_E_DEVICE);
-  for (size_t l = 0; l + 1 < f->level_ptr.size(); l++) {
-    int64_t most = 0;
-    for (int64_t j = f->level_ptr[l]; j < f->level_ptr[l + 1]; j++)
-      most = std::max(most, pp[j + 1] - pp[j]);
-    level_pairs.push_back(most);
-  }
-  const hipError_t le =
-      launch_dual(f, level_pairs, (int32_t)Beff, (int32_t)W, objective, D, dst, e0, e1, s);
-  if (le != hipSuccess) {
-    set_last_error("dual table launch", le);
-    return finish(RC_E_DEVICE);
-  }
-  DevStatus hs;
-  if (hipMemcpyAsync(&hs, dst, sizeof(hs), hipMemcpyDeviceToHost, s) != hipSuccess ||
-      hipStreamSynchronize(s) != hipSuccess)
-    return finish(RC_E_DEVICE);
-  const bool schedule = k || chain_host || seg_host || cached_host || overhead || peak || cache_mem;
-  if (schedule && hs.t_sel >= 0) {
-    const int n = f->g->n;
-    int32_t* chain_d = A.get_n<int32_t>(f->F);
-    int32_t* seg_d = A.get_n<int32_t>(n);
-    uint8_t* cached_d = A.get_n<uint8_t>(n);
-    if (!chain_d || !seg_d || !cached_d) return finish(RC_E_NOMEM);
-    const hipError_t te = launch_dual_trace(f, (int32_t)Beff, (int32_t)W, objective, D, dst,
-                                            chain_d, seg_d, cached_d, s);
-    if (te != hipSuccess) {
-      set_last_error("dual traceback launch", te);
-      return finish(RC_E_DEVICE);
-    }
-    std::vector<int32_t> ch(f->F), sg(n);
-    std::vector<uint8_t> ca(n);
-    DevStatus ts;
-    if (hipMemcpyAsync(&ts, dst, sizeof(ts), hipMemcpyDeviceToHost, s) != hipSuccess ||
-        hipMemcpyAsync(ch.data(), chain_d, sizeof(int32_t) * f->F, hipMemcpyDeviceToHost, s) !=
-            hipSuccess ||
-        (n > 0 &&
-         (hipMemcpyAsync(sg.data(), seg_d, sizeof(int32_t) * n, hipMemcpyDeviceToHost, s) !=
-              hipSuccess ||
-          hipMemcpyAsync(ca.data(), cached_d, n, hipMemcpyDeviceToHost, s) != hipSuccess)) ||
-        hipStreamSynchronize(s) != hipSuccess)
-      return finish(RC_E_DEVICE);
-    if (ts.error || ts.k < 0 || ts.k > f->F) {
-      set_last_error_msg("dual traceback: the walk did not end at (empty set, 0, 0)");
-      return finish(RC_E_DEVICE);
-    }
-    if (k) *k = ts.k;
-    if (chain_host) std::copy(ch.begin(), ch.begin() + ts.k, chain_host);
-    if (seg_host) std::copy(sg.begin(), sg.end(), seg_host);
-    if (cached_host) std::copy(ca.begin(), ca.end(), cached_host);
-    if (overhead) *overhead = ts.overhead;
-    if (peak) *peak = ts.peak;
-    if (cache_mem) *cache_mem = ts.cache_mem;
-  }
-  if (fill_ms) {
+  const int st = dual_solve(f, objective, buf, e0, e1, s, t_opt, m_opt, k, chain_host, seg_host,
+                            cached_host, overhead, peak, cache_mem);
+  if (fill_ms && st >= 0) {
     float ms = -1.f;
     if (hipEventElapsedTime(&ms, e0, e1) != hipSuccess) ms = -1.f;
     *fill_ms = ms;
   }
-  if (t_opt) *t_opt = hs.t_sel;
-  if (m_opt) *m_opt = hs.t_sel >= 0 ? hs.m_sel : -1;
-  return finish(hs.t_sel >= 0 ? RC_OK : RC_INFEASIBLE);
+  return finish(st);
 }
 
 int rc_family_sets(rc_family f, uint64_t* bits_host, void* stream) {

@@ -131,6 +131,7 @@ struct rc_family_s {
   uint32_t* bmin_scratch = nullptr; // rc_min_budget: f values of large families
   // host copies used for launches
   std::vector<int64_t> level_ptr; // family index ranges of equal set size
+  std::vector<int64_t> level_pairs; // the most pairs of a target in each level
   std::vector<int32_t> level_maxw;
   std::vector<int32_t> w_host;
   std::vector<int64_t> row_off_host;
@@ -283,6 +284,23 @@ hipError_t launch_dual(rc_family f, const std::vector<int64_t>& level_pairs, int
                        int objective, uint32_t* D, DevStatus* st, hipEvent_t e0, hipEvent_t e1,
                        hipStream_t s);
 int64_t blocked_columns(rc_family f);
+
+// One memory-indexed solve (rc_api.hip): the sizes it needs and the device
+// buffers it runs in (the caller's arena, or the static scratch of the
+// allocation-free entry point).
+struct DualBuffers {
+  int64_t Beff = 0, W = 0, cells = 0;
+  uint32_t* D = nullptr;          // [cells]
+  DevStatus* st = nullptr;
+  int32_t* chain = nullptr;       // [F]
+  int32_t* seg = nullptr;         // [n]
+  uint8_t* cached = nullptr;      // [n]
+};
+int dual_buffers(rc_family f, int64_t B, int32_t objective, DualBuffers* out);
+int dual_solve(rc_family f, int32_t objective, const DualBuffers& b, hipEvent_t e0,
+               hipEvent_t e1, hipStream_t s, int64_t* t_opt, int64_t* m_opt, int32_t* k,
+               int32_t* chain_host, int32_t* seg_host, uint8_t* cached_host, int64_t* overhead,
+               int64_t* peak, int64_t* cache_mem);
 hipError_t launch_fill_blocked(rc_solution sol, hipStream_t s);
 
 }  // namespace rcdp

@@ -86,16 +86,16 @@ int peak_valu(int kind, int blocks, int iters, void* out, float* ms, double* ops
   if (blocks <= 0 || iters <= 0 || !out || !ms || !ops || (kind != 0 && kind != 1)) return -1;
   hipEvent_t e0, e1;
   if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) return -1;
-  hipEventRecord(e0, 0);
+  (void)hipEventRecord(e0, 0);
   if (kind == 0)
     hipLaunchKernelGGL(k_valu_i32, dim3(blocks), dim3(256), 0, 0, (uint32_t*)out, iters, 12345u);
   else
     hipLaunchKernelGGL(k_valu_pk_u16, dim3(blocks), dim3(256), 0, 0, (uint32_t*)out, iters,
                        12345u);
-  hipEventRecord(e1, 0);
+  (void)hipEventRecord(e1, 0);
   int st = hipGetLastError() == hipSuccess ? timed(e0, e1, ms) : -1;
-  hipEventDestroy(e0);
-  hipEventDestroy(e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
   *ops = (double)blocks * 256.0 * iters * kUnroll * kChains * 2 * (kind == 1 ? 2 : 1);
   return st;
 }
@@ -105,13 +105,13 @@ int peak_copy(const void* src, void* dst, int64_t bytes, int blocks, float* ms) 
   if (!src || !dst || bytes <= 0 || bytes % 16 || blocks <= 0 || !ms) return -1;
   hipEvent_t e0, e1;
   if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) return -1;
-  hipEventRecord(e0, 0);
+  (void)hipEventRecord(e0, 0);
   hipLaunchKernelGGL(k_copy, dim3(blocks), dim3(256), 0, 0, (const uint4*)src, (uint4*)dst,
                      bytes / 16);
-  hipEventRecord(e1, 0);
+  (void)hipEventRecord(e1, 0);
   int st = hipGetLastError() == hipSuccess ? timed(e0, e1, ms) : -1;
-  hipEventDestroy(e0);
-  hipEventDestroy(e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
   return st;
 }
 
