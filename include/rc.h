@@ -70,7 +70,8 @@ enum rc_status {
   RC_E_OVERFLOW = -5,       /* a value exceeds the table's integer widths */
   RC_E_NOMEM = -6,          /* the allocator returned NULL */
   RC_E_DEVICE = -7,         /* a HIP call failed or a kernel reported an error */
-  RC_E_STATE = -9           /* the handle is in the wrong state for the call */
+  RC_E_STATE = -9,          /* the handle is in the wrong state for the call */
+  RC_E_SCRATCH = -10        /* the allocation-free entry point's scratch is too small */
 };
 
 /* Family statistics (rc_family_info).
@@ -174,6 +175,28 @@ int rc_solve_dual(rc_family f, int64_t B, int32_t objective, void* stream, int64
                   int64_t* m_opt, float* fill_ms, int32_t* k, int32_t* chain_host,
                   int32_t* seg_host, uint8_t* cached_host, int64_t* overhead, int64_t* peak,
                   int64_t* cache_mem);
+/*
+ * rc_solve_dual_noalloc -- rc_solve_dual without any allocation, for callers
+ * that cannot allocate device memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc.  It calls no hipMalloc,
+ * hipFree, event creation or allocating routine; the table, the status block
+ * and the schedule buffers live in a file-scope device array of 16 MiB that
+ * every GPU the library runs on holds until the process ends.  The family
+ * (built beforehand with rc_build_family) and the host outputs are the
+ * caller's, as with rc_solve_dual.
+ *  Arguments, outputs and results as rc_solve_dual (no fill_ms).  The
+ *  scratch takes 256 + 4 (num_sets + n) + n bytes plus the table's
+ *  num_sets * (min(B, 2 M(V), M(V)) + 1) * 4 bytes, each part rounded up to
+ *  256 bytes; a larger solve returns RC_E_SCRATCH and does nothing.
+ *  Calls on one GPU share its scratch: calls that overlap on one GPU (other
+ *  threads or streams) race and must be serialised by the caller.
+ * Returns RC_OK, RC_INFEASIBLE, RC_E_ARG, RC_E_OVERFLOW, RC_E_SCRATCH,
+ * RC_E_DEVICE.
+ */
+int rc_solve_dual_noalloc(rc_family f, int64_t B, int32_t objective, void* stream,
+                          int64_t* t_opt, int64_t* m_opt, int32_t* k, int32_t* chain_host,
+                          int32_t* seg_host, uint8_t* cached_host, int64_t* overhead,
+                          int64_t* peak, int64_t* cache_mem);
 void rc_family_free(rc_family f);
 
 /*

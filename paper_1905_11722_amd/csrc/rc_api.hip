@@ -175,6 +175,7 @@ const char* rc_status_str(int status) {
     case RC_E_NOMEM: return "device allocation failed";
     case RC_E_DEVICE: return "HIP runtime or kernel error";
     case RC_E_STATE: return "handle in the wrong state";
+    case RC_E_SCRATCH: return "the solve needs more than the allocation-free scratch";
     default: return "unknown status";
   }
 }

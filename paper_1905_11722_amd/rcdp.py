@@ -28,6 +28,7 @@ LIB_PATH = os.path.join(HERE, "librcdp.so")
 OK, INFEASIBLE = 0, 1
 E_ARG, E_CYCLE, E_COST, E_TOO_MANY_SETS, E_OVERFLOW, E_NOMEM, E_DEVICE, E_STATE = (
     -1, -2, -3, -4, -5, -6, -7, -9)
+E_SCRATCH = -10
 MODES = {"exact": 0, "pruned": 1}
 OBJECTIVES = {"tc": 0, "mc": 1}
 
@@ -99,6 +100,11 @@ def load_library():
     lib.rc_solve_dual.argtypes = [P, i64, i32, P, ctypes.POINTER(i64), ctypes.POINTER(i64),
                                   ctypes.POINTER(ctypes.c_float), ctypes.POINTER(i32), P, P, P,
                                   ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i64)]
+    lib.rc_solve_dual_noalloc.restype = ctypes.c_int
+    lib.rc_solve_dual_noalloc.argtypes = [P, i64, i32, P, ctypes.POINTER(i64),
+                                          ctypes.POINTER(i64), ctypes.POINTER(i32), P, P, P,
+                                          ctypes.POINTER(i64), ctypes.POINTER(i64),
+                                          ctypes.POINTER(i64)]
     lib.rc_solution_fill_kernel_ms.restype = ctypes.c_int
     lib.rc_solution_fill_kernel_ms.argtypes = [P, ctypes.POINTER(ctypes.c_float)]
     lib.rc_reconstruct.restype = ctypes.c_int
@@ -280,6 +286,29 @@ class Family:
         return t.value, m.value, ms.value, Schedule(
             chain[:k.value].copy(), seg[:n].copy(), cached[:n].astype(bool), o.value, p.value,
             c.value)
+
+    def solve_dual_noalloc(self, B, objective="tc"):
+        """(t, m, Schedule or None) from rc_solve_dual_noalloc: the
+        memory-indexed solve with its schedule, run in the library's static
+        scratch instead of allocated memory."""
+        lib = load_library()
+        F = self.info["num_sets"]
+        n = self.graph.n
+        t, m, k = ctypes.c_int64(-1), ctypes.c_int64(-1), ctypes.c_int32(-1)
+        chain = np.zeros(max(F, 1), dtype=np.int32)
+        seg = np.zeros(max(n, 1), dtype=np.int32)
+        cached = np.zeros(max(n, 1), dtype=np.uint8)
+        o, p, c = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+        st = lib.rc_solve_dual_noalloc(self._h, int(B), OBJECTIVES.get(objective, objective),
+                                       _stream(), ctypes.byref(t), ctypes.byref(m),
+                                       ctypes.byref(k), chain.ctypes.data, seg.ctypes.data,
+                                       cached.ctypes.data, ctypes.byref(o), ctypes.byref(p),
+                                       ctypes.byref(c))
+        _check(st, "rc_solve_dual_noalloc", allow=(OK, INFEASIBLE))
+        if st == INFEASIBLE:
+            return t.value, m.value, None
+        return t.value, m.value, Schedule(chain[:k.value].copy(), seg[:n].copy(),
+                                          cached[:n].astype(bool), o.value, p.value, c.value)
 
     def sweep(self, budgets, objective="mc"):
         """Solve at every budget in one batched fill (rc_solve_batch):
