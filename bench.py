@@ -34,24 +34,32 @@ if ROOT not in sys.path:
 VALU_INT32_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
 VALU_U16_PEAK_TOPS = 2 * VALU_INT32_PEAK_TOPS
 OPS_PER_RELAXATION = 3          # compare with tau, add dm, min into the target
-# The sources that shape the row-push fill kernel and its traffic: the
+# The sources that shape each wavefront fill kernel and its traffic: the
 # kernel, its record preparation, the shared helpers and constants.
-FILL_SOURCES = ["paper_1905_11722_amd/csrc/blocked.hip", "paper_1905_11722_amd/csrc/blocks.hip",
-                "paper_1905_11722_amd/csrc/wavefront.h", "paper_1905_11722_amd/csrc/rc_internal.h"]
+_CSRC = "paper_1905_11722_amd/csrc/"
+FILL_SOURCES = {
+    "k_fill_blocked": [_CSRC + "blocked.hip", _CSRC + "blocks.hip", _CSRC + "wavefront.h",
+                       _CSRC + "rc_internal.h"],
+    "k_fill_wide": [_CSRC + "wide.hip", _CSRC + "blocks.hip", _CSRC + "wavefront.h",
+                    _CSRC + "rc_internal.h"],
+    "k_fill_ghost": [_CSRC + "ghost.hip", _CSRC + "blocks.hip", _CSRC + "wavefront.h",
+                     _CSRC + "rc_internal.h", _CSRC + "ghost_cut.h"],
+    "k_fill_level": [_CSRC + "fill.hip", _CSRC + "rc_internal.h"],
+}
 
 
-def fill_source_hash():
+def fill_source_hash(kernel):
     h = hashlib.sha256()
-    for rel in FILL_SOURCES:
+    for rel in FILL_SOURCES[kernel]:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def read_traffic(workload):
-    """HBM traffic of the fill from committed rocprofv3 PMC runs, if they were
-    taken on the current fill source; else None."""
-    path = os.path.join(ROOT, "profiles", f"k_fill_blocked_{workload}_traffic.txt")
+def read_traffic(kernel, workload):
+    """HBM traffic of the fill kernel from committed rocprofv3 PMC runs, if
+    they were taken on the current source of that kernel; else None."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.txt")
     if not os.path.exists(path):
         return None
     rec = {}
@@ -60,7 +68,7 @@ def read_traffic(workload):
             if "=" in line and not line.startswith((" ", "#", "`")):
                 k, v = line.split("=", 1)
                 rec[k.strip()] = v.strip()
-    if rec.get("fill_source_sha256_16") != fill_source_hash():
+    if rec.get("fill_source_sha256_16") != fill_source_hash(kernel):
         return None
     try:
         return int(rec["hbm_bytes_per_launch"])
@@ -74,11 +82,12 @@ def run_step(rcdp, g, case):
     sched = sol.reconstruct() if sol.feasible else None
     fill_ms = sol.fill_ms()
     kernel_ms = sol.fill_kernel_ms()
+    kernel = sol.fill_kernel()
     info = fam.info
     t_star = sol.t_star
     sol.free()
     fam.free()
-    return info, fill_ms, kernel_ms, t_star, sched
+    return info, fill_ms, kernel_ms, t_star, sched, kernel
 
 
 def time_phases(rcdp, torch, case, steps):
@@ -116,7 +125,7 @@ def time_case(rcdp, torch, case, steps, warmup):
     fills, kernels = [], []
     t0 = time.perf_counter()
     for _ in range(steps):
-        info, fill_ms, kernel_ms, t_star, sched = run_step(rcdp, g, case)
+        info, fill_ms, kernel_ms, t_star, sched, kernel = run_step(rcdp, g, case)
         fills.append(fill_ms)
         kernels.append(kernel_ms)
     torch.cuda.synchronize()
@@ -135,6 +144,7 @@ def time_case(rcdp, torch, case, steps, warmup):
         "info": info,
         "t_star": t_star,
         "k": None if sched is None else int(len(sched.chain)),
+        "kernel": kernel,
     }
 
 
@@ -473,10 +483,9 @@ def main():
             "peak": VALU_U16_PEAK_TOPS,
             "unit": "TOP/s (packed 16-bit integer VALU)",
             "frac": achieved / VALU_U16_PEAK_TOPS,
-            "traffic": read_traffic(case.name),
+            "traffic": read_traffic(main_res["kernel"], case.name),
             "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE)",
-            "kernel": "k_fill_blocked (one launch per solve; the level path's launches "
-                      "when the family takes that path)",
+            "kernel": main_res["kernel"],
             "kernel_ms": main_res["kernel_ms"],
             "ops_per_relaxation": OPS_PER_RELAXATION,
             "frac_of_int32_peak": achieved / VALU_INT32_PEAK_TOPS,

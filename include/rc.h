@@ -37,6 +37,26 @@
  *    size (ascending numeric value sum_{v in L} 2^v), and through it which of
  *    several equally good predecessors the traceback follows (the smallest
  *    family index, as with the strict update of Algorithm 1).
+ *
+ * Environment switches (read when a family is built or a table is solved;
+ * none changes a result, only which kernels compute it and how they are
+ * shaped; an unrecognised value is ignored):
+ *  - RCDP_FILL = level | wavefront | wide | ghost: the fill of Algorithm 1.
+ *    level: one launch per group of equal-size sets (k_fill_level).
+ *    wavefront: the persistent row-push wavefront over fixed blocks of
+ *    targets (k_fill_blocked).  wide: the split-panel wavefront over fixed
+ *    blocks (k_fill_wide).  ghost: the wavefront over ghost-zone blocks
+ *    (k_fill_ghost; families of at most 4096 sets).  Unset: chosen from the
+ *    family's size, width and number of levels (rc_solution_fill_path
+ *    reports the choice).
+ *  - RCDP_WIDE_NP = 3 | 4: panel waves per workgroup of k_fill_wide
+ *    (default 3).
+ *  - RCDP_CPT = 1 | 2 | 4: cells per thread of a k_fill_blocked column
+ *    (default from the table's width).
+ *  - RCDP_GHOST_CPT = 1 | 2: cells per thread of a k_fill_ghost column
+ *    (default from the table's width).
+ *  - RCDP_DEBUG (any value): the wavefront fills print their launch shape
+ *    to stderr.
  */
 #ifndef RC_H
 #define RC_H
@@ -257,6 +277,12 @@ int rc_solution_fill_ms(rc_solution s, float* ms);
  * which runs one launch per group of equal-size sets, this equals
  * rc_solution_fill_ms.  Returns RC_OK or RC_E_ARG (NULL argument). */
 int rc_solution_fill_kernel_ms(rc_solution s, float* ms);
+/* Which fill the solve ran (all of them compute the same table, Algorithm 1
+ * of Section 4.2): *path = 0 one launch per group of equal-size sets
+ * (k_fill_level), 1 the persistent row-push wavefront (k_fill_blocked), 2
+ * the ghost-zone wavefront (k_fill_ghost), 3 the split-panel wavefront
+ * (k_fill_wide).  Returns RC_OK or RC_E_ARG (NULL argument). */
+int rc_solution_fill_path(rc_solution s, int32_t* path);
 
 /*
  * rc_reconstruct -- trace optarg back from (V, t*) (Section 4.2) and

@@ -488,18 +488,18 @@ __global__ void k_fill_pending(uint4* p, int64_t n16) {
     p[x] = make_uint4(v, v, v, v);
 }
 
-// Left padding of every row (cells of its 64-cell-aligned slot before the
-// row) and an 8-cell sentinel hold infinity, so that 16-byte window loads
-// that touch them read infinity.
-__global__ void k_pad_init(int64_t F, const int32_t* w, const int64_t* row_off, uint16_t* m,
-                           uint16_t* sentinel) {
-  for (int64_t s = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; s < F;
-       s += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t pad = ((int64_t)w[s] + kRowAlign - 1) / kRowAlign * kRowAlign;
-    const int64_t start = row_off[s] + w[s] - pad;
-    for (int64_t x = start; x < row_off[s]; x++) m[x] = (uint16_t)kInfM;
+// The padding of every row (the cells of its slot before the row, at least
+// kGuard of them), the kGuard cells after the last row and an 8-cell
+// sentinel hold infinity, so that window loads that touch them read
+// infinity.  One workgroup per row.
+__global__ void k_pad_init(int64_t F, const int32_t* w, const int64_t* row_off, int64_t cells,
+                           uint16_t* m, uint16_t* sentinel) {
+  for (int64_t s = blockIdx.x; s <= F; s += gridDim.x) {
+    const int64_t start = s < F ? row_off[s] + w[s] - row_slot(w[s]) : cells;
+    const int64_t end = s < F ? row_off[s] : cells + kGuard;
+    for (int64_t x = start + threadIdx.x; x < end; x += blockDim.x) m[x] = (uint16_t)kInfM;
   }
-  if (blockIdx.x == 0 && threadIdx.x < 8) sentinel[threadIdx.x] = (uint16_t)kInfM;
+  if (blockIdx.x == 0 && threadIdx.x < 8 && sentinel) sentinel[threadIdx.x] = (uint16_t)kInfM;
 }
 
 }  // namespace
@@ -527,14 +527,15 @@ hipError_t launch_push_prepare(rc_solution sol, int32_t C, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Cells [64, cells) (row 0 is the first row and fills one 64-cell line).
+// Cells after row 0's slot (row 0, the empty set, holds its one cell).
 hipError_t launch_fill_pending(rc_solution sol, hipStream_t s) {
   rc_family f = sol->f;
-  const int64_t n16 = (f->cells - kRowAlign) / 8;
+  const int64_t first = row_slot(1);                 // slot 0 holds the empty set's row
+  const int64_t n16 = (f->cells - first) / 8;
   if (n16 <= 0) return hipSuccess;
   const unsigned grid = (unsigned)std::min<int64_t>((n16 + 255) / 256, 4096);
   hipLaunchKernelGGL(k_fill_pending, dim3(grid), dim3(256), 0, s,
-                     reinterpret_cast<uint4*>(sol->m + kRowAlign), n16);
+                     reinterpret_cast<uint4*>(sol->m + first), n16);
   return hipGetLastError();
 }
 
@@ -546,9 +547,9 @@ hipError_t launch_blk_clusters(rc_family f, int64_t* count, hipStream_t s) {
 
 hipError_t launch_pad_init(rc_solution sol, hipStream_t s) {
   rc_family f = sol->f;
-  const unsigned grid = (unsigned)std::min<int64_t>((f->F + 255) / 256, 1024);
-  hipLaunchKernelGGL(k_pad_init, dim3(grid > 0 ? grid : 1), dim3(256), 0, s, f->F, f->w,
-                     f->row_off, sol->m, sol->sentinel);
+  const unsigned grid = (unsigned)std::min<int64_t>(f->F + 1, 4096);
+  hipLaunchKernelGGL(k_pad_init, dim3(grid), dim3(256), 0, s, f->F, f->w, f->row_off, f->cells,
+                     sol->m, sol->sentinel);
   return hipGetLastError();
 }
 

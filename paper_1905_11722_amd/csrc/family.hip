@@ -561,18 +561,16 @@ __global__ __launch_bounds__(256) void k_set_quantities_lanes(
 
 __global__ void k_row_widths(int64_t F, const int32_t* w, int64_t* padded) {
   const int64_t s = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-  if (s < F) padded[s] = ((int64_t)w[s] + kRowAlign - 1) / kRowAlign * kRowAlign;
+  if (s < F) padded[s] = row_slot(w[s]);
 }
 
 // Rows are right-aligned inside their padded slots: row s ends on a
 // kRowAlign boundary, so every column counted from the row end is made of
-// whole 128-byte lines.
+// whole 128-byte lines, and at least kGuard padding cells separate it from
+// the previous row.
 __global__ void k_row_align(int64_t F, const int32_t* w, int64_t* row_off) {
   const int64_t s = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-  if (s < F) {
-    const int64_t pad = ((int64_t)w[s] + kRowAlign - 1) / kRowAlign * kRowAlign;
-    row_off[s] += pad - w[s];
-  }
+  if (s < F) row_off[s] += row_slot(w[s]) - w[s];
 }
 
 // ------------------------------------------------------------------ pairs

@@ -313,7 +313,9 @@ static int32_t family_block_kind(rc_family f, bool shape_known) {
   const int64_t F = f->F;
   if (F < 2) return 0;
   const char* env = std::getenv("RCDP_FILL");
-  if (F > kGhostMaxSets || (env && std::strcmp(env, "wavefront") == 0)) return kBlocksFixed;
+  if (F > kGhostMaxSets ||
+      (env && (std::strcmp(env, "wavefront") == 0 || std::strcmp(env, "wide") == 0)))
+    return kBlocksFixed;
   if (env && std::strcmp(env, "ghost") == 0) return kBlocksGhost;
   if (!shape_known) return -1;                 // decided once the table's shape is known
   const bool wide_many = f->max_row >= 65536 && f->level_ptr.size() > 101;
@@ -475,6 +477,7 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
   RC_HIP(hipStreamSynchronize(s));
   if (hs.error) return RC_E_DEVICE;
   f->cells = f->row_off_host[F];
+  f->cells_alloc = f->cells + kGuard;
   if (f->cells >= ((int64_t)1 << 40)) return RC_E_OVERFLOW;
   f->level_ptr.clear();
   f->level_maxw.clear();
@@ -529,8 +532,25 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
     RC_HIP(launch_scan(counts, f->clu_ptr, f->nblk, 1, s));
     RC_HIP(hipMemcpyAsync(&f->clu_total, f->clu_ptr + f->nblk, sizeof(int64_t),
                           hipMemcpyDeviceToHost, s));
+    // the split-panel fill: one record per (block, source, shift), a block's
+    // records sorted in LDS, byte offsets of the table in 31 bits
+    std::vector<int64_t> wcount;
+    if (f->blk_kind == kBlocksFixed) {
+      f->wrec_ptr = A.get_n<int64_t>(f->nblk + 1);
+      if (!f->wrec_ptr) return RC_E_NOMEM;
+      RC_HIP(launch_wide_count(f, counts, s));
+      wcount.resize((size_t)f->nblk);
+      RC_HIP(hipMemcpyAsync(wcount.data(), counts, sizeof(int64_t) * (size_t)f->nblk,
+                            hipMemcpyDeviceToHost, s));
+      RC_HIP(launch_scan(counts, f->wrec_ptr, f->nblk, 1, s));
+      RC_HIP(hipMemcpyAsync(&f->wrec_total, f->wrec_ptr + f->nblk, sizeof(int64_t),
+                            hipMemcpyDeviceToHost, s));
+    }
     RC_HIP(hipStreamSynchronize(s));
     f->has_records = true;
+    f->has_wide = f->blk_kind == kBlocksFixed && 2 * f->cells_alloc < INT32_MAX &&
+                  f->wrec_total < ((int64_t)1 << 26);
+    for (int64_t x : wcount) f->has_wide = f->has_wide && x <= kWMaxRec;
   }
   return RC_OK;
 }
@@ -666,15 +686,18 @@ static void destroy_events(rc_solution sol) {
 
 static int choose_fill_path(rc_family f) {
   if (!f->has_records || f->F < 2) return 0;
-  const int wide = f->blk_kind == kBlocksGhost ? 2 : 1;   // the family's wavefront fill
+  // the family's wavefront fill: ghost-zone blocks, or fixed blocks of kJB
+  // with the split-panel fill when it can take the family
+  const int wide = f->blk_kind == kBlocksGhost ? 2 : (f->has_wide ? 3 : 1);
   const char* env = std::getenv("RCDP_FILL");
   if (env && std::strcmp(env, "level") == 0) return 0;
-  if (env && (std::strcmp(env, "wavefront") == 0 || std::strcmp(env, "ghost") == 0)) return wide;
+  if (env && std::strcmp(env, "wavefront") == 0 && f->blk_kind == kBlocksFixed) return 1;
+  if (env && (std::strcmp(env, "wide") == 0 || std::strcmp(env, "ghost") == 0)) return wide;
   // the ghost-zone fill measured at least as fast as the level launches on
-  // every workload shape; the row-push fill only pays off on wide tables of
-  // many levels, where one persistent launch beats one launch per level
+  // every workload shape; the fixed-block fills only pay off on wide tables
+  // of many levels, where one persistent launch beats one launch per level
   if (wide == 2) return 2;
-  return (f->max_row >= 8192 && f->level_ptr.size() > 100) ? 1 : 0;
+  return (f->max_row >= 8192 && f->level_ptr.size() > 100) ? wide : 0;
 }
 
 }  // extern "C"
@@ -701,7 +724,7 @@ static int new_solution(rc_family f, int64_t B, int32_t objective, rc_solution* 
     delete sol;
     return st;
   };
-  sol->m = sol->arena.get_n<uint16_t>(f->cells);
+  sol->m = sol->arena.get_n<uint16_t>(f->cells_alloc);
   sol->status = sol->arena.get_n<DevStatus>(1);
   sol->chain = sol->arena.get_n<int32_t>(f->F);
   sol->seg = sol->arena.get_n<int32_t>(f->g->n);
@@ -714,7 +737,22 @@ static int new_solution(rc_family f, int64_t B, int32_t objective, rc_solution* 
   if (sol->fill_path != 0 &&
       (hipEventCreate(&sol->evk0) != hipSuccess || hipEventCreate(&sol->evk1) != hipSuccess))
     return fail(RC_E_DEVICE);
-  if (sol->fill_path != 0) {
+  if (sol->fill_path == 3) {
+    const int64_t K = wide_columns(f), R = f->wrec_total;
+    sol->progress = sol->arena.get_n<int32_t>(K);
+    sol->ticket = sol->arena.get_n<int32_t>(1);
+    sol->wkey = sol->arena.get_n<int64_t>(R);
+    sol->wbl_tmp = sol->arena.get_n<int32_t>(2 * R);
+    sol->wtd_tmp = sol->arena.get_n<int32_t>(kWTd * R);
+    sol->wbl = sol->arena.get_n<int32_t>(2 * (R + kWPad));
+    sol->wtd = sol->arena.get_n<int32_t>(kWTd * (R + kWPad));
+    sol->wmeta = sol->arena.get_n<int32_t>(f->nblk * kWMeta);
+    sol->wlive = sol->arena.get_n<int32_t>(f->nblk * K);
+    sol->wpush = sol->arena.get_n<int32_t>(f->nblk * kJB * kWPush);
+    if (!sol->progress || !sol->ticket || !sol->wkey || !sol->wbl_tmp || !sol->wtd_tmp ||
+        !sol->wbl || !sol->wtd || !sol->wmeta || !sol->wlive || !sol->wpush)
+      return fail(RC_E_NOMEM);
+  } else if (sol->fill_path != 0) {
     const int64_t K = sol->fill_path == 2 ? ghost_columns(f) : blocked_columns(f);
     sol->progress = sol->arena.get_n<int32_t>(K);
     sol->ticket = sol->arena.get_n<int32_t>(1);
@@ -786,11 +824,13 @@ static int solve_one(rc_family f, int64_t B, int32_t objective, void* stream, rc
   if (dominance && !(we = sol->arena.get_n<int32_t>(f->F))) return fail(RC_E_NOMEM);
   if (hipEventRecord(sol->ev0, s) != hipSuccess) return fail(RC_E_DEVICE);
   const hipError_t fe = dominance               ? launch_fill_dominance(sol, we, s)
+                        : sol->fill_path == 3   ? launch_fill_wide(sol, s)
                         : sol->fill_path == 2   ? launch_fill_ghost(sol, s)
                         : sol->fill_path == 1 ? launch_fill_blocked(sol, s)
                                               : launch_fill(sol, s);
   if (fe != hipSuccess) {
-    set_last_error(sol->fill_path == 2   ? "ghost fill launch"
+    set_last_error(sol->fill_path == 3   ? "split-panel fill launch"
+                   : sol->fill_path == 2 ? "ghost fill launch"
                    : sol->fill_path == 1 ? "blocked fill launch"
                                          : "level fill launch",
                    fe);
@@ -846,7 +886,17 @@ int rc_solve_batch(rc_family f, const int64_t* B_host, int32_t nb, int32_t objec
   if (hipEventRecord(s0->ev0, s) != hipSuccess) return fail(RC_E_DEVICE);
   std::vector<BParams> host_prm;
   std::vector<GParams> host_gprm;
-  if (s0->fill_path == 2) {
+  std::vector<WParams> host_wprm;
+  if (s0->fill_path == 3) {
+    host_wprm.resize((size_t)nb);
+    WParams* dev_prm = s0->arena.get_n<WParams>(nb);
+    if (!dev_prm) return fail(RC_E_NOMEM);
+    const hipError_t fe = launch_fill_wide_batch(sols.data(), nb, host_wprm.data(), dev_prm, s);
+    if (fe != hipSuccess) {
+      set_last_error("batched split-panel fill launch", fe);
+      return fail(RC_E_DEVICE);
+    }
+  } else if (s0->fill_path == 2) {
     host_gprm.resize((size_t)nb);
     GParams* dev_prm = s0->arena.get_n<GParams>(nb);
     if (!dev_prm) return fail(RC_E_NOMEM);
@@ -908,6 +958,12 @@ int rc_solution_fill_kernel_ms(rc_solution s, float* ms) {
   return RC_OK;
 }
 
+int rc_solution_fill_path(rc_solution s, int32_t* path) {
+  if (!s || !path) return RC_E_ARG;
+  *path = s->fill_path;
+  return RC_OK;
+}
+
 int rc_reconstruct(rc_solution sol, void* stream, int32_t* k, int32_t* chain_host,
                    int32_t* seg_host, uint8_t* cached_host, int64_t* overhead, int64_t* peak,
                    int64_t* cache_mem) {
@@ -948,7 +1004,7 @@ int rc_export_table(rc_solution sol, int64_t first, int64_t count, int64_t* m_ho
   hipStream_t s = as_stream(stream);
   const int64_t W = f->g->T_total + 1;
   if (arg_host && !sol->arg) {               // optarg of the whole table, derived once
-    sol->arg = sol->arena.get_n<uint16_t>(f->cells);
+    sol->arg = sol->arena.get_n<uint16_t>(f->cells_alloc);
     if (!sol->arg) return RC_E_NOMEM;
     RC_HIP(launch_arg_all(sol, s));
   }

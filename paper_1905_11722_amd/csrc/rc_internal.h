@@ -17,7 +17,10 @@ constexpr int kMaxWords = kMaxNodes / 64;
 constexpr int kMaxSets = 65535;                 // family index fits 16 bits
 constexpr uint32_t kInfM = 0xFFFFu;             // opt = infinity in a 16-bit cell
 constexpr uint32_t kNoArg = 0xFFFFu;            // optarg = none
-constexpr int64_t kRowAlign = 64;               // cells; rows start on 128-byte lines
+constexpr int64_t kRowAlign = 64;               // cells; rows end on 128-byte lines
+constexpr int64_t kGuard = 256;                 // infinite cells before every row and after
+                                                // the last one (a 256-cell window that
+                                                // overlaps a row reads no other row)
 constexpr int kJB = 8;                          // blocked fill: targets per block
 constexpr int64_t kMaxRecords = (int64_t)1 << 21;  // blocked fill: cap on panel records
 constexpr int kRecInts = 32;                    // blocked fill: int32 per compact record
@@ -38,6 +41,31 @@ constexpr int kGhostHalo = 64;                  // ghost-zone fill: cells recomp
 constexpr int kGhostMaxSets = 4096;             // ghost-zone fill: largest family it takes
 constexpr int kNear = kJB;                      // ghost cut: predecessors j-1 .. j-kNear examined
 constexpr int kTriInts = 16;                    // ghost-zone fill: int32 per (block, row) list
+constexpr int kWC = 256;                        // split-panel fill: cells per column
+constexpr int kWH = 512;                        // split-panel fill: halo cells of a row push
+constexpr int kWTd = 8;                         // split-panel fill: int32 budgets + additions
+constexpr int kWPad = 64;                       // split-panel fill: records read past the end
+constexpr int kWMeta = 8;                       // split-panel fill: int32 per block
+constexpr int kWMaxRec = 4096;                  // split-panel fill: records of one block
+constexpr int kWPush = 64;                      // split-panel fill: int32 per (block, row) list
+// layout of a split-panel push list (one row of a block and its 16 target slots:
+// the later rows of its block, then the rows of the next block)
+constexpr int kWpE = 0;                         // [16] shift of each slot, -1 = no live pair
+constexpr int kWpTau = 16;                      // [8] budgets of slots 2q, 2q+1 (uint16 pairs)
+constexpr int kWpDm = 24;                       // [8] additions of slots 2q, 2q+1
+constexpr int kWpP = 32;                        // P_j of the row
+constexpr int kWpEnd = 33;                      // [2] index of the row's cell u = 0
+constexpr int kWpEmax = 35;                     // largest live shift
+constexpr int kWpMaxPt = 36;                    // largest P of a live target (-1 none)
+constexpr int kWpHalo = 37;                     // halo cells to stage (multiple of 64)
+constexpr int kWpFar = 38;                      // bit mask of slots with shift > kWH
+constexpr int kWpNear = 39;                     // bit mask of slot pairs with a shift <= kWH
+
+// Cells of row slot s: the row's w cells right-aligned on a kRowAlign
+// boundary, preceded by at least kGuard padding cells (infinity).
+__host__ __device__ inline int64_t row_slot(int64_t w) {
+  return (w + kRowAlign - 1) / kRowAlign * kRowAlign + kGuard;
+}
 
 // Device allocator with ownership tracking.
 struct Arena {
@@ -104,6 +132,7 @@ struct rc_family_s {
   rc_graph g = nullptr;
   int32_t mode = 0;
   int64_t F = 0, P = 0, cells = 0, relax = 0, max_row = 0;
+  int64_t cells_alloc = 0;        // cells + kGuard: the table with its trailing guard
   int64_t fstride = 0;            // stride of the word-major bitmask arrays
   rcdp::Arena arena;
   // device: family, word-major [words][fstride]
@@ -126,6 +155,9 @@ struct rc_family_s {
   int64_t* rec_ptr = nullptr;     // [nblk+1]
   int64_t* clu_ptr = nullptr;     // [nblk+1] compact records (shift clusters) per block
   int64_t clu_total = 0;
+  int64_t* wrec_ptr = nullptr;    // [nblk+1] split-panel records per block (upper bound)
+  int64_t wrec_total = 0;
+  bool has_wide = false;          // the split-panel fill can take this family
   rcdp::BlockRecords rec;
   rcdp::DevStatus* status = nullptr;
   uint32_t* bmin_scratch = nullptr; // rc_min_budget: f values of large families
@@ -159,9 +191,18 @@ struct rc_solution_s {
   int32_t* blk_meta = nullptr;    // blocked fill: per block metadata [nblk * kMetaInts]
   int32_t* push = nullptr;        // blocked fill: row push lists [nblk * kJB * kPushInts]
   int32_t* tri = nullptr;         // ghost-zone fill: in-block lists [nblk * kJB * kTriInts]
+  int64_t* wkey = nullptr;        // split-panel fill: sort keys of the unsorted records
+  int32_t* wbl_tmp = nullptr;     // split-panel fill: unsorted window base / limit
+  int32_t* wtd_tmp = nullptr;     // split-panel fill: unsorted budgets / additions
+  int32_t* wbl = nullptr;         // split-panel fill: [2 (R + kWPad)] sorted
+  int32_t* wtd = nullptr;         // split-panel fill: [kWTd (R + kWPad)] sorted
+  int32_t* wmeta = nullptr;       // split-panel fill: [nblk * kWMeta]
+  int32_t* wlive = nullptr;       // split-panel fill: [nblk * K] records reaching each column
+  int32_t* wpush = nullptr;       // split-panel fill: [nblk * kJB * kWPush]
   int32_t cpt = 1;                // blocked fill: cells per thread of a column
   uint16_t* sentinel = nullptr;   // 8 cells of infinity
-  int32_t fill_path = 0;          // 0 level launches, 1 row-push wavefront, 2 ghost-zone wavefront
+  int32_t fill_path = 0;          // 0 level launches, 1 row-push wavefront, 2 ghost-zone
+                                  // wavefront, 3 split-panel wavefront
   hipEvent_t ev0 = nullptr, ev1 = nullptr;    // around the whole fill
   hipEvent_t evk0 = nullptr, evk1 = nullptr;  // around the wavefront kernel alone
   float fill_ms = 0.f;
@@ -302,5 +343,34 @@ int dual_solve(rc_family f, int32_t objective, const DualBuffers& b, hipEvent_t 
                int32_t* chain_host, int32_t* seg_host, uint8_t* cached_host, int64_t* overhead,
                int64_t* peak, int64_t* cache_mem);
 hipError_t launch_fill_blocked(rc_solution sol, hipStream_t s);
+
+
+// ---- split-panel wavefront fill (wide.hip)
+// Kernel parameters of one table.
+struct WParams {
+  int32_t F;
+  int32_t nblk;
+  int32_t K;                             // columns of kWC cells
+  int32_t rec_cap;                       // records of the family (upper bound)
+  const int32_t* meta;                   // [nblk * kWMeta]
+  const int64_t* rptr;                   // [nblk + 1] first record of each block
+  const int32_t* live;                   // [nblk * K] records reaching each column
+  const int32_t* bl;                     // [2 (R + kWPad)] window base / limit (bytes)
+  const int32_t* td;                     // [kWTd (R + kWPad)] budgets / additions
+  const int32_t* push;                   // [nblk * kJB * kWPush]
+  uint16_t* m;
+  int64_t m_bytes;                       // the table with its trailing guard
+  int32_t null_off;                      // byte offset of the trailing guard
+  int32_t pad0;
+  int32_t* progress;
+  int32_t* ticket;
+  DevStatus* st;
+  int64_t timeout_ticks;
+};
+int64_t wide_columns(rc_family f);
+hipError_t launch_wide_count(rc_family f, int64_t* count, hipStream_t s);
+hipError_t launch_fill_wide(rc_solution sol, hipStream_t s);
+hipError_t launch_fill_wide_batch(rc_solution* sols, int32_t nb, WParams* host_prm,
+                                  WParams* dev_prm, hipStream_t s);
 
 }  // namespace rcdp

@@ -107,6 +107,8 @@ def load_library():
                                           ctypes.POINTER(i64)]
     lib.rc_solution_fill_kernel_ms.restype = ctypes.c_int
     lib.rc_solution_fill_kernel_ms.argtypes = [P, ctypes.POINTER(ctypes.c_float)]
+    lib.rc_solution_fill_path.restype = ctypes.c_int
+    lib.rc_solution_fill_path.argtypes = [P, ctypes.POINTER(ctypes.c_int32)]
     lib.rc_reconstruct.restype = ctypes.c_int
     lib.rc_reconstruct.argtypes = [P, P, ctypes.POINTER(i32), P, P, P, ctypes.POINTER(i64),
                                    ctypes.POINTER(i64), ctypes.POINTER(i64)]
@@ -386,6 +388,15 @@ class Solution:
         _check(load_library().rc_solution_fill_kernel_ms(self._h, ctypes.byref(ms)),
                "rc_solution_fill_kernel_ms")
         return ms.value
+
+    FILL_KERNELS = ("k_fill_level", "k_fill_blocked", "k_fill_ghost", "k_fill_wide")
+
+    def fill_kernel(self):
+        """Name of the fill kernel the solve ran (see rc_solution_fill_path)."""
+        path = ctypes.c_int32()
+        _check(load_library().rc_solution_fill_path(self._h, ctypes.byref(path)),
+               "rc_solution_fill_path")
+        return self.FILL_KERNELS[path.value]
 
     def reconstruct(self):
         lib = load_library()

@@ -185,11 +185,13 @@ def test_full_size_cases(rc, oracle_mod, name):
 # ---------------------------------------------------------------- fill paths
 # The library picks a persistent wavefront fill for wide tables and
 # per-level launches for narrow ones; RCDP_FILL forces one: "level", the
-# row-push wavefront ("wavefront", fixed blocks of 8 targets) or the
-# ghost-zone wavefront ("ghost", blocks cut to fit its recomputed halo).
-# Rows wider than one column make the wavefront's cross-workgroup waits real.
+# row-push wavefront ("wavefront", fixed blocks of 8 targets), the
+# split-panel wavefront ("wide", fixed blocks, panel records shared among
+# waves) or the ghost-zone wavefront ("ghost", blocks cut to fit its
+# recomputed halo).  Rows wider than one column make the wavefront's
+# cross-workgroup waits real.
 
-PATHS = ["level", "wavefront", "ghost"]
+PATHS = ["level", "wavefront", "wide", "ghost"]
 
 WIDE = [(n, p, seed) for seed, (n, p) in enumerate(
     [(n, p) for n in (4, 6, 8, 10, 12) for p in (0.2, 0.45, 0.7)])]
@@ -214,6 +216,31 @@ def test_fill_paths_small_cases(rc, oracle_mod, monkeypatch, path, name):
     g = c.graph
     for B in (c.B, 2 * max(g.M), sum(g.M), 2 * sum(g.M)):
         compare(rc, oracle_mod, g, c.mode, B)
+
+
+@pytest.mark.parametrize("path,kernel", [("level", "k_fill_level"),
+                                         ("wavefront", "k_fill_blocked"),
+                                         ("wide", "k_fill_wide"), ("ghost", "k_fill_ghost")])
+def test_fill_path_is_reported(rc, monkeypatch, path, kernel):
+    """rc_solution_fill_path names the fill a forced RCDP_FILL ran."""
+    monkeypatch.setenv("RCDP_FILL", path)
+    g = W.random_dag(10, 0.45, 5007, tmax=700, mmax=60)
+    fam = rc.Graph.create(g).build_family("exact")
+    sol = fam.solve(2 * sum(g.M), "tc")
+    assert sol.fill_kernel() == kernel
+    sol.free()
+
+
+@pytest.mark.parametrize("n,p,seed", WIDE[::2])
+def test_wide_fill_four_panel_waves(rc, oracle_mod, monkeypatch, n, p, seed):
+    """The split-panel fill with four panel waves per workgroup."""
+    monkeypatch.setenv("RCDP_FILL", "wide")
+    monkeypatch.setenv("RCDP_WIDE_NP", "4")
+    g = W.random_dag(n, p, 8000 + seed, tmax=900, mmax=60)
+    lo, hi = 2 * max(g.M), 2 * sum(g.M)
+    for B in (lo, (lo + hi) // 2, hi):
+        for mode in ("exact", "pruned"):
+            compare(rc, oracle_mod, g, mode, B)
 
 
 @pytest.mark.parametrize("cpt", ["1", "2", "4"])
@@ -243,7 +270,7 @@ def test_ghost_column_widths(rc, oracle_mod, monkeypatch, cpt, n, p, seed):
             compare(rc, oracle_mod, g, mode, B)
 
 
-@pytest.mark.parametrize("path", ["wavefront", "ghost"])
+@pytest.mark.parametrize("path", ["wavefront", "wide", "ghost"])
 @pytest.mark.parametrize("seed", [10, 12, 16])
 def test_wavefront_repeated_solves(rc, oracle_mod, monkeypatch, path, seed):
     """The same wide tables solved repeatedly: the persistent fill's columns
