@@ -222,10 +222,17 @@ __global__ __launch_bounds__(kFillThreads) void k_arg_all(
 }
 
 // t* = min (time-centric) or max (memory-centric) finite t of row V.
-// Each wave reduces its cells' candidate first and issues one atomic, so
-// that a row of mostly finite cells does not serialize on one address.
-__global__ void k_select(const uint16_t* m, const int64_t* row_off, int64_t v, const int32_t* w,
-                         int objective, DevStatus* st) {
+// A few workgroups stride over the row, reduce within the wave and then the
+// workgroup, and issue one atomic each (one atomic per wave serialised on
+// the one address).
+constexpr int kSelectThreads = 256;
+constexpr int kSelectBlocks = 64;
+
+__global__ __launch_bounds__(kSelectThreads) void k_select(const uint16_t* m,
+                                                          const int64_t* row_off, int64_t v,
+                                                          const int32_t* w, int objective,
+                                                          DevStatus* st) {
+  __shared__ int32_t s_best[kSelectThreads / kWave];
   const int64_t off = row_off[v];
   const int32_t wv = w[v];
   const bool tc = objective == RC_TIME_CENTRIC;
@@ -236,11 +243,17 @@ __global__ void k_select(const uint16_t* m, const int64_t* row_off, int64_t v, c
     const int32_t y = __shfl_xor(best, o, kWave);
     best = tc ? min(best, y) : max(best, y);
   }
-  if ((threadIdx.x & (kWave - 1)) == 0 && (tc ? best != INT32_MAX : best >= 0)) {
-    if (tc)
-      atomicMin(&st->t_sel, best);
-    else
-      atomicMax(&st->t_sel, best);
+  if ((threadIdx.x & (kWave - 1)) == 0) s_best[threadIdx.x / kWave] = best;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int q = 1; q < kSelectThreads / kWave; q++)
+      best = tc ? min(best, s_best[q]) : max(best, s_best[q]);
+    if (tc ? best != INT32_MAX : best >= 0) {
+      if (tc)
+        atomicMin(&st->t_sel, best);
+      else
+        atomicMax(&st->t_sel, best);
+    }
   }
 }
 
@@ -427,9 +440,10 @@ hipError_t launch_select(rc_solution sol, hipStream_t s) {
   rc_family f = sol->f;
   const int64_t v = f->F - 1;
   const int64_t wv = f->w_host[v];
-  const unsigned blocks = (unsigned)std::min<int64_t>((wv + 255) / 256, 1024);
-  hipLaunchKernelGGL(k_select, dim3(blocks > 0 ? blocks : 1), dim3(256), 0, s, sol->m, f->row_off,
-                     v, f->w, sol->objective, sol->status);
+  const unsigned blocks =
+      (unsigned)std::min<int64_t>((wv + kSelectThreads - 1) / kSelectThreads, kSelectBlocks);
+  hipLaunchKernelGGL(k_select, dim3(blocks > 0 ? blocks : 1), dim3(kSelectThreads), 0, s, sol->m,
+                     f->row_off, v, f->w, sol->objective, sol->status);
   hipLaunchKernelGGL(k_select_finish, dim3(1), dim3(64), 0, s, sol->m, f->row_off, v,
                      sol->status);
   return hipGetLastError();

@@ -278,10 +278,14 @@ int rc_graph_create(int32_t n, const int32_t* row_ptr, const int32_t* col_idx, c
   if (st == RC_OK) {
     g->dSucc = g->arena.get_n<uint64_t>((int64_t)n * g->words);
     g->dPred = g->arena.get_n<uint64_t>((int64_t)n * g->words);
-    if (!g->dSucc || !g->dPred) st = RC_E_NOMEM;
+    g->dAnc = g->arena.get_n<uint64_t>((int64_t)n * g->words);
+    if (!g->dSucc || !g->dPred || !g->dAnc) st = RC_E_NOMEM;
   }
   if (st == RC_OK && n > 0 && launch_graph_masks(g, d_row_ptr, d_col_idx, s) != hipSuccess)
     st = RC_E_DEVICE;
+  // the ancestor sets (Section 4.3's generators of the pruned family) are a
+  // property of the graph: computed once here, read by every pruned family
+  if (st == RC_OK && n > 0 && launch_ancestors(g, g->dAnc, s) != hipSuccess) st = RC_E_DEVICE;
   // the host vectors above must stay alive until the copies have completed
   if (st == RC_OK && hipStreamSynchronize(s) != hipSuccess) st = RC_E_DEVICE;
   if (st != RC_OK) {
@@ -383,10 +387,7 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
   f->bits = A.get_n<uint64_t>(cap * words);
   if (!cand || !lvl || !f->bits) return RC_E_NOMEM;
   if (f->mode == RC_FAMILY_PRUNED) {
-    uint64_t* anc = tmp.get_n<uint64_t>((int64_t)n * words);
-    if (!anc) return RC_E_NOMEM;
-    if (n > 0) RC_HIP(launch_ancestors(g, anc, s));
-    RC_HIP(launch_pruned_candidates(g, anc, cand, s));
+    RC_HIP(launch_pruned_candidates(g, g->dAnc, cand, s));
   } else {
     RC_HIP(launch_enum_exact(g, cand, cap, lvl, f->status, s));
   }

@@ -126,6 +126,8 @@ struct rc_graph_s {
   int32_t* dByDepth = nullptr;    // nodes sorted by depth (longest path from a source)
   int32_t* dDepthPtr = nullptr;   // [num_depths+1]
   int32_t num_depths = 0;
+  uint64_t* dAnc = nullptr;       // [n][words] ancestors of each node (without the node),
+                                  // the pruned family's generators, computed once per graph
 };
 
 struct rc_family_s {
