@@ -228,9 +228,12 @@ void rc_family_free(rc_family f);
  *  objective RC_TIME_CENTRIC: t* = min{t : opt[V, t] finite};
  *    RC_MEMORY_CENTRIC: t* = max{t : opt[V, t] finite} (Section 4.4).
  *  *t_opt, *m_opt: t* and opt[V, t*], or -1 and -1 when infeasible.
+ * Cells are 16 bits wide while min(B, 2 M(V)) <= 65532 (every fill path);
+ * above that the table takes 32-bit cells and the one-launch-per-level fill
+ * (rc_solution_fill_path reports 0), with the same results.
  * Returns RC_OK or RC_INFEASIBLE (both create *out, whose table can be
- * exported), or an error: RC_E_ARG, RC_E_OVERFLOW (min(B, 2 M(V)) > 65532),
- * RC_E_NOMEM, RC_E_DEVICE.
+ * exported), or an error: RC_E_ARG, RC_E_OVERFLOW (min(B, 2 M(V)) > 2^30,
+ * which rc_graph_create's limit on M(V) rules out), RC_E_NOMEM, RC_E_DEVICE.
  */
 int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solution* out,
              int64_t* t_opt, int64_t* m_opt);
@@ -247,7 +250,8 @@ int rc_solve(rc_family f, int64_t B, int32_t objective, void* stream, rc_solutio
  *  front as rc_solve's table), infinity elsewhere; the optarg of a front
  *  cell and the schedule of rc_reconstruct follow Algorithm 1 with the skip
  *  (the smallest family index among the sources that are propagated).
- *  Other arguments, handles and errors as rc_solve.
+ *  Other arguments, handles and errors as rc_solve, except that the skip
+ *  takes 16-bit cells only: RC_E_OVERFLOW when min(B, 2 M(V)) > 65532.
  */
 int rc_solve_dominance(rc_family f, int64_t B, void* stream, rc_solution* out, int64_t* t_opt,
                        int64_t* m_opt);

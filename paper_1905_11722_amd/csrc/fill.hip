@@ -6,7 +6,9 @@
 // t = 0 .. w_L - 1 (w_L = T(L \ boundary(L)) + 1; every cell beyond is
 // provably infinite, since each recomputed node of a chain ending at L lies
 // in L \ boundary(L)).  Rows are contiguous in t and end on 128-byte
-// lines.  A cell stores m = opt[L, t] as uint16 (0xFFFF = infinity).
+// lines.  A cell stores m = opt[L, t] as uint16 (0xFFFF = infinity), or
+// as uint32 (0xFFFFFFFF = infinity) for budgets beyond the 16-bit range
+// (the level fill, selection, traceback and export take either width).
 //
 // Pull form of Algorithm 1: opt[L', t'] is the minimum over predecessors
 // L (proper subsets of L' in the family) of opt[L, t' - dt] + dm, taken
@@ -35,6 +37,12 @@ constexpr int kFillThreads = 256;
 constexpr int kCellsPerThread = 4;
 constexpr int kTile = kFillThreads * kCellsPerThread;
 
+// Infinity of a table of cells of type T.
+template <class T>
+__device__ __forceinline__ constexpr uint32_t cell_inf() {
+  return sizeof(T) == 2 ? 0xFFFFu : 0xFFFFFFFFu;
+}
+
 __device__ __forceinline__ int64_t wave_sum_i64(int64_t x) {
   for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, kWave);
   return x;
@@ -50,8 +58,8 @@ __device__ __forceinline__ int64_t word_cost(uint64_t bits, int word, const int3
 }
 
 // opt[empty, 0] = 0 (Algorithm 1's initial condition); selection state.
-__global__ void k_solve_init(uint16_t* m, const int64_t* row_off, int objective,
-                             DevStatus* st) {
+template <class T>
+__global__ void k_solve_init(T* m, const int64_t* row_off, int objective, DevStatus* st) {
   if (threadIdx.x == 0) {
     m[row_off[0]] = 0;
     st->error = 0;
@@ -67,19 +75,20 @@ __global__ void k_solve_init(uint16_t* m, const int64_t* row_off, int objective,
 // so that every source read and every store of a wave is contiguous.
 // ws[i]: the source row's cells that may be read, t < ws[i] (its width w[i],
 // or the end of its weak front under the dominance skip).
+template <class T>
 __global__ __launch_bounds__(kFillThreads) void k_fill_level(
     int64_t lb, const int32_t* __restrict__ w, const int64_t* __restrict__ row_off,
     const int64_t* __restrict__ pred_ptr, const int32_t* __restrict__ pidx,
     const int32_t* __restrict__ pdt, const int32_t* __restrict__ pdm,
     const int32_t* __restrict__ pc, int32_t Beff, const int32_t* __restrict__ ws,
-    uint16_t* __restrict__ m) {
+    T* __restrict__ m) {
   const int64_t j = lb + blockIdx.y;
   const int32_t wj = w[j];
   const int32_t tile0 = blockIdx.x * kTile;
   if (tile0 >= wj) return;
   uint32_t acc[kCellsPerThread];
 #pragma unroll
-  for (int r = 0; r < kCellsPerThread; r++) acc[r] = kInfM;
+  for (int r = 0; r < kCellsPerThread; r++) acc[r] = cell_inf<T>();
   const int64_t p0 = pred_ptr[j], p1 = pred_ptr[j + 1];
   for (int64_t p = p0; p < p1; ++p) {
     // budget test of Algorithm 1: opt[L, t] + c <= B, i.e. opt[L, t] <= tau
@@ -89,7 +98,7 @@ __global__ __launch_bounds__(kFillThreads) void k_fill_level(
     const int32_t i = pidx[p];
     const int32_t wi = ws[i];                 // cells of the source row that can be read
     if (dt >= tile0 + kTile || dt + wi <= tile0) continue;  // window misses the tile
-    const uint16_t* src = m + row_off[i];
+    const T* src = m + row_off[i];
     const uint32_t dm = (uint32_t)pdm[p];
 #pragma unroll
     for (int r = 0; r < kCellsPerThread; r++) {
@@ -100,11 +109,11 @@ __global__ __launch_bounds__(kFillThreads) void k_fill_level(
       }
     }
   }
-  uint16_t* mo = m + row_off[j];
+  T* mo = m + row_off[j];
 #pragma unroll
   for (int r = 0; r < kCellsPerThread; r++) {
     const int32_t tp = tile0 + r * kFillThreads + (int32_t)threadIdx.x;
-    if (tp < wj) mo[tp] = (uint16_t)acc[r];
+    if (tp < wj) mo[tp] = (T)acc[r];
   }
 }
 
@@ -194,11 +203,12 @@ __global__ __launch_bounds__(kFillThreads) void k_front(
 // optarg of every cell of targets [lb, lb + gridDim.y) from the final
 // table: the smallest predecessor index whose cell passes the budget test
 // and reproduces the target value (Algorithm 1's first writer).
+template <class T>
 __global__ __launch_bounds__(kFillThreads) void k_arg_all(
     int64_t lb, const int32_t* __restrict__ w, const int64_t* __restrict__ row_off,
     const int64_t* __restrict__ pred_ptr, const int32_t* __restrict__ pidx,
     const int32_t* __restrict__ pdt, const int32_t* __restrict__ pdm,
-    const int32_t* __restrict__ pc, int32_t Beff, const uint16_t* __restrict__ m,
+    const int32_t* __restrict__ pc, int32_t Beff, const T* __restrict__ m,
     uint16_t* __restrict__ arg) {
   const int64_t j = lb + blockIdx.y;
   const int32_t wj = w[j];
@@ -206,13 +216,14 @@ __global__ __launch_bounds__(kFillThreads) void k_arg_all(
   if (tp >= wj) return;
   const uint32_t mj = m[row_off[j] + tp];
   uint32_t a = kNoArg;
-  if (mj != kInfM && j > 0) {
+  if (mj != cell_inf<T>() && j > 0) {
     for (int64_t p = pred_ptr[j]; p < pred_ptr[j + 1]; ++p) {
       const int32_t t = tp - pdt[p];
       const int32_t i = pidx[p];
       if ((uint32_t)t >= (uint32_t)w[i]) continue;
-      const int32_t x = m[row_off[i] + t];
-      if (x <= Beff - pc[p] && (uint32_t)(x + pdm[p]) == mj) {
+      const uint32_t x = m[row_off[i] + t];
+      if (x != cell_inf<T>() && (int64_t)x <= (int64_t)Beff - pc[p] &&
+          (uint32_t)(x + pdm[p]) == mj) {
         a = (uint32_t)i;
         break;
       }
@@ -228,17 +239,17 @@ __global__ __launch_bounds__(kFillThreads) void k_arg_all(
 constexpr int kSelectThreads = 256;
 constexpr int kSelectBlocks = 64;
 
-__global__ __launch_bounds__(kSelectThreads) void k_select(const uint16_t* m,
-                                                          const int64_t* row_off, int64_t v,
-                                                          const int32_t* w, int objective,
-                                                          DevStatus* st) {
+template <class T>
+__global__ __launch_bounds__(kSelectThreads) void k_select(const T* m, const int64_t* row_off,
+                                                          int64_t v, const int32_t* w,
+                                                          int objective, DevStatus* st) {
   __shared__ int32_t s_best[kSelectThreads / kWave];
   const int64_t off = row_off[v];
   const int32_t wv = w[v];
   const bool tc = objective == RC_TIME_CENTRIC;
   int32_t best = tc ? INT32_MAX : -1;
   for (int32_t t = blockIdx.x * blockDim.x + threadIdx.x; t < wv; t += gridDim.x * blockDim.x)
-    if (m[off + t] != kInfM) best = tc ? min(best, t) : max(best, t);
+    if (m[off + t] != cell_inf<T>()) best = tc ? min(best, t) : max(best, t);
   for (int o = kWave / 2; o > 0; o >>= 1) {
     const int32_t y = __shfl_xor(best, o, kWave);
     best = tc ? min(best, y) : max(best, y);
@@ -257,8 +268,8 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(const uint16_t* m,
   }
 }
 
-__global__ void k_select_finish(const uint16_t* m, const int64_t* row_off, int64_t v,
-                                DevStatus* st) {
+template <class T>
+__global__ void k_select_finish(const T* m, const int64_t* row_off, int64_t v, DevStatus* st) {
   if (threadIdx.x != 0) return;
   if (st->t_sel == INT32_MAX) st->t_sel = -1;
   st->m_sel = st->t_sel >= 0 ? (int32_t)m[row_off[v] + st->t_sel] : -1;
@@ -274,7 +285,7 @@ __global__ void k_select_finish(const uint16_t* m, const int64_t* row_off, int64
 constexpr int kTraceThreads = 512;
 constexpr int kTraceLds = 2048;       // families up to this size keep their per-set arrays in LDS
 
-template <bool kLds>
+template <bool kLds, class Cell>
 __global__ __launch_bounds__(kTraceThreads) void k_trace(
     int64_t F, int n, int words, int64_t fstride, const uint64_t* __restrict__ bits,
     const uint64_t* __restrict__ bd, const int32_t* __restrict__ A, const int32_t* __restrict__ T,
@@ -282,7 +293,7 @@ __global__ __launch_bounds__(kTraceThreads) void k_trace(
     const int64_t* __restrict__ row_off, const int64_t* __restrict__ pred_ptr,
     const int32_t* __restrict__ pidx, const int32_t* __restrict__ pdt,
     const int32_t* __restrict__ pdm, const int32_t* __restrict__ pc, int32_t Beff,
-    const uint16_t* __restrict__ m, int64_t T_total, DevStatus* st, int32_t* chain, int32_t* seg,
+    const Cell* __restrict__ m, int64_t T_total, DevStatus* st, int32_t* chain, int32_t* seg,
     uint8_t* cached) {
   // per-set arrays of small families live in LDS for the whole walk
   __shared__ int32_t s_w[kTraceLds];
@@ -345,8 +356,9 @@ __global__ __launch_bounds__(kTraceThreads) void k_trace(
       const int32_t i = pidx[pq], dt = pdt[pq], c = pc[pq], dm = pdm[pq];
       const int64_t ts = t - dt;
       const bool inrow = valid && ts >= 0 && ts < Wd(i);
-      const int32_t x = m[Off(i) + (inrow ? ts : 0)];
-      const bool hit = inrow && x <= Beff - c && (uint32_t)(x + dm) == mj;
+      const uint32_t x = m[Off(i) + (inrow ? ts : 0)];
+      const bool hit = inrow && x != cell_inf<Cell>() && (int64_t)x <= (int64_t)Beff - c &&
+                       (uint32_t)(x + dm) == mj;
       const unsigned long long bal = __ballot(hit);
       if (lane == 0) s_first[par][wave] = bal ? wave * kWave + __ffsll((long long)bal) - 1 : INT32_MAX;
       s_src[par][tid] = i;
@@ -361,7 +373,7 @@ __global__ __launch_bounds__(kTraceThreads) void k_trace(
       }
       par ^= 1;
     }
-    if (next_i < 0 || mj == kInfM) {
+    if (next_i < 0 || mj == cell_inf<Cell>()) {
       bad = true;
       break;
     }
@@ -387,22 +399,34 @@ __global__ __launch_bounds__(kTraceThreads) void k_trace(
 
 hipError_t launch_solve_init(rc_solution sol, hipStream_t s) {
   rc_family f = sol->f;
-  hipLaunchKernelGGL(k_solve_init, dim3(1), dim3(64), 0, s, sol->m, f->row_off,
-                     sol->objective, sol->status);
+  if (sol->cell32)
+    hipLaunchKernelGGL(k_solve_init<uint32_t>, dim3(1), dim3(64), 0, s, sol->m32, f->row_off,
+                       sol->objective, sol->status);
+  else
+    hipLaunchKernelGGL(k_solve_init<uint16_t>, dim3(1), dim3(64), 0, s, sol->m, f->row_off,
+                       sol->objective, sol->status);
   return hipGetLastError();
 }
 
-hipError_t launch_fill(rc_solution sol, hipStream_t s) {
+template <class T>
+static void fill_levels(rc_solution sol, T* m, hipStream_t s) {
   rc_family f = sol->f;
   const int64_t L = (int64_t)f->level_ptr.size() - 1;
   for (int64_t l = 1; l < L; l++) {            // level 0 is the empty set
     const int64_t lb = f->level_ptr[l], le = f->level_ptr[l + 1];
     const int64_t tiles = (f->level_maxw[l] + kTile - 1) / kTile;
     if (tiles <= 0 || le <= lb) continue;
-    hipLaunchKernelGGL(k_fill_level, dim3((unsigned)tiles, (unsigned)(le - lb)),
+    hipLaunchKernelGGL(k_fill_level<T>, dim3((unsigned)tiles, (unsigned)(le - lb)),
                        dim3(kFillThreads), 0, s, lb, f->w, f->row_off, f->pred_ptr, f->pidx,
-                       f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, f->w, sol->m);
+                       f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, f->w, m);
   }
+}
+
+hipError_t launch_fill(rc_solution sol, hipStream_t s) {
+  if (sol->cell32)
+    fill_levels(sol, sol->m32, s);
+  else
+    fill_levels(sol, sol->m, s);
   return hipGetLastError();
 }
 
@@ -428,7 +452,7 @@ hipError_t launch_fill_dominance(rc_solution sol, int32_t* we, hipStream_t s) {
     const int64_t lb = f->level_ptr[l], le = f->level_ptr[l + 1];
     const int64_t tiles = (f->level_maxw[l] + kTile - 1) / kTile;
     if (tiles <= 0 || le <= lb) continue;
-    hipLaunchKernelGGL(k_fill_level, dim3((unsigned)tiles, (unsigned)(le - lb)),
+    hipLaunchKernelGGL(k_fill_level<uint16_t>, dim3((unsigned)tiles, (unsigned)(le - lb)),
                        dim3(kFillThreads), 0, s, lb, f->w, f->row_off, f->pred_ptr, f->pidx,
                        f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, (const int32_t*)we, sol->m);
     front(lb, le - lb, f->level_maxw[l]);
@@ -436,46 +460,70 @@ hipError_t launch_fill_dominance(rc_solution sol, int32_t* we, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_select(rc_solution sol, hipStream_t s) {
+template <class T>
+static void select_t(rc_solution sol, const T* m, hipStream_t s) {
   rc_family f = sol->f;
   const int64_t v = f->F - 1;
   const int64_t wv = f->w_host[v];
   const unsigned blocks =
       (unsigned)std::min<int64_t>((wv + kSelectThreads - 1) / kSelectThreads, kSelectBlocks);
-  hipLaunchKernelGGL(k_select, dim3(blocks > 0 ? blocks : 1), dim3(kSelectThreads), 0, s, sol->m,
+  hipLaunchKernelGGL(k_select<T>, dim3(blocks > 0 ? blocks : 1), dim3(kSelectThreads), 0, s, m,
                      f->row_off, v, f->w, sol->objective, sol->status);
-  hipLaunchKernelGGL(k_select_finish, dim3(1), dim3(64), 0, s, sol->m, f->row_off, v,
-                     sol->status);
+  hipLaunchKernelGGL(k_select_finish<T>, dim3(1), dim3(64), 0, s, m, f->row_off, v, sol->status);
+}
+
+hipError_t launch_select(rc_solution sol, hipStream_t s) {
+  if (sol->cell32)
+    select_t<uint32_t>(sol, sol->m32, s);
+  else
+    select_t<uint16_t>(sol, sol->m, s);
   return hipGetLastError();
 }
 
-hipError_t launch_trace(rc_solution sol, hipStream_t s) {
+template <class T>
+static void trace_t(rc_solution sol, const T* m, hipStream_t s) {
   rc_family f = sol->f;
   rc_graph g = f->g;
   if (f->F <= kTraceLds)
-    hipLaunchKernelGGL(k_trace<true>, dim3(1), dim3(kTraceThreads), 0, s, f->F, g->n, g->words,
+    hipLaunchKernelGGL((k_trace<true, T>), dim3(1), dim3(kTraceThreads), 0, s, f->F, g->n, g->words,
                        f->fstride, f->bits, f->bd, f->A, g->dT, g->dM, f->w, f->row_off,
-                       f->pred_ptr, f->pidx, f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, sol->m,
+                       f->pred_ptr, f->pidx, f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, m,
                        g->T_total, sol->status, sol->chain, sol->seg, sol->cached);
   else
-    hipLaunchKernelGGL(k_trace<false>, dim3(1), dim3(kTraceThreads), 0, s, f->F, g->n, g->words,
-                       f->fstride, f->bits, f->bd, f->A, g->dT, g->dM, f->w, f->row_off,
-                       f->pred_ptr, f->pidx, f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, sol->m,
-                       g->T_total, sol->status, sol->chain, sol->seg, sol->cached);
+    hipLaunchKernelGGL((k_trace<false, T>), dim3(1), dim3(kTraceThreads), 0, s, f->F, g->n,
+                       g->words, f->fstride, f->bits, f->bd, f->A, g->dT, g->dM, f->w,
+                       f->row_off, f->pred_ptr, f->pidx, f->pdt, f->pdm, f->pc,
+                       (int32_t)sol->Beff, m, g->T_total, sol->status, sol->chain, sol->seg,
+                       sol->cached);
+}
+
+hipError_t launch_trace(rc_solution sol, hipStream_t s) {
+  if (sol->cell32)
+    trace_t<uint32_t>(sol, sol->m32, s);
+  else
+    trace_t<uint16_t>(sol, sol->m, s);
   return hipGetLastError();
 }
 
-hipError_t launch_arg_all(rc_solution sol, hipStream_t s) {
+template <class T>
+static void arg_all_t(rc_solution sol, const T* m, hipStream_t s) {
   rc_family f = sol->f;
   const int64_t L = (int64_t)f->level_ptr.size() - 1;
   for (int64_t l = 0; l < L; l++) {
     const int64_t lb = f->level_ptr[l], le = f->level_ptr[l + 1];
     const int64_t tiles = (f->level_maxw[l] + kFillThreads - 1) / kFillThreads;
     if (tiles <= 0 || le <= lb) continue;
-    hipLaunchKernelGGL(k_arg_all, dim3((unsigned)tiles, (unsigned)(le - lb)), dim3(kFillThreads),
-                       0, s, lb, f->w, f->row_off, f->pred_ptr, f->pidx, f->pdt, f->pdm, f->pc,
-                       (int32_t)sol->Beff, sol->m, sol->arg);
+    hipLaunchKernelGGL(k_arg_all<T>, dim3((unsigned)tiles, (unsigned)(le - lb)),
+                       dim3(kFillThreads), 0, s, lb, f->w, f->row_off, f->pred_ptr, f->pidx,
+                       f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, m, sol->arg);
   }
+}
+
+hipError_t launch_arg_all(rc_solution sol, hipStream_t s) {
+  if (sol->cell32)
+    arg_all_t<uint32_t>(sol, sol->m32, s);
+  else
+    arg_all_t<uint16_t>(sol, sol->m, s);
   return hipGetLastError();
 }
 

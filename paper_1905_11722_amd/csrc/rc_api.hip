@@ -310,8 +310,9 @@ void rc_graph_free(rc_graph g) {
 // Which blocks the family's wavefront records use.  RCDP_FILL=wavefront
 // forces the row-push fill's fixed blocks and RCDP_FILL=ghost the ghost-zone
 // blocks (families of at most kGhostMaxSets sets).  Otherwise: fixed blocks
-// for families beyond that size and for wide tables of many levels (where
-// the row-push fill measured faster), ghost-zone blocks for the rest.
+// for families beyond that size and for tables with rows of 2^16 cells and
+// more (where the split-panel fill measured fastest), ghost-zone blocks for
+// the rest.
 // shape_known: max_row and the levels are set (after the host copies).
 static int32_t family_block_kind(rc_family f, bool shape_known) {
   const int64_t F = f->F;
@@ -322,8 +323,9 @@ static int32_t family_block_kind(rc_family f, bool shape_known) {
     return kBlocksFixed;
   if (env && std::strcmp(env, "ghost") == 0) return kBlocksGhost;
   if (!shape_known) return -1;                 // decided once the table's shape is known
-  const bool wide_many = f->max_row >= 65536 && f->level_ptr.size() > 101;
-  return wide_many ? kBlocksFixed : kBlocksGhost;
+  // rows of 2^16 cells and more: fixed blocks, so that the split-panel fill
+  // (measured fastest on every such table here) can take the family
+  return f->max_row >= 65536 ? kBlocksFixed : kBlocksGhost;
 }
 
 // Block starts of the chosen kind (host).
@@ -695,9 +697,11 @@ static int choose_fill_path(rc_family f) {
   if (env && std::strcmp(env, "wavefront") == 0 && f->blk_kind == kBlocksFixed) return 1;
   if (env && (std::strcmp(env, "wide") == 0 || std::strcmp(env, "ghost") == 0)) return wide;
   // the ghost-zone fill measured at least as fast as the level launches on
-  // every workload shape; the fixed-block fills only pay off on wide tables
-  // of many levels, where one persistent launch beats one launch per level
+  // every workload shape; the fixed-block fills pay off on tables with rows
+  // of 2^16 cells and more, and on wide tables of many levels, where one
+  // persistent launch beats one launch per level
   if (wide == 2) return 2;
+  if (f->max_row >= 65536) return wide;
   return (f->max_row >= 8192 && f->level_ptr.size() > 100) ? wide : 0;
 }
 
@@ -709,7 +713,9 @@ static int new_solution(rc_family f, int64_t B, int32_t objective, rc_solution* 
   if (!f || B < 0) return RC_E_ARG;
   if (objective != RC_TIME_CENTRIC && objective != RC_MEMORY_CENTRIC) return RC_E_ARG;
   const int64_t Beff = std::min<int64_t>(B, 2 * f->g->M_total);
-  if (Beff > kMaxBudget) return RC_E_OVERFLOW;
+  if (Beff > kMaxBudget32) return RC_E_OVERFLOW;
+  // a budget beyond the 16-bit cells: 32-bit cells and the level fill
+  const bool cell32 = Beff > kMaxBudget;
   rc_solution sol = new (std::nothrow) rc_solution_s();
   if (!sol) return RC_E_NOMEM;
   sol->f = f;
@@ -725,16 +731,20 @@ static int new_solution(rc_family f, int64_t B, int32_t objective, rc_solution* 
     delete sol;
     return st;
   };
-  sol->m = sol->arena.get_n<uint16_t>(f->cells_alloc);
+  sol->cell32 = cell32;
+  if (cell32)
+    sol->m32 = sol->arena.get_n<uint32_t>(f->cells_alloc);
+  else
+    sol->m = sol->arena.get_n<uint16_t>(f->cells_alloc);
   sol->status = sol->arena.get_n<DevStatus>(1);
   sol->chain = sol->arena.get_n<int32_t>(f->F);
   sol->seg = sol->arena.get_n<int32_t>(f->g->n);
   sol->cached = sol->arena.get_n<uint8_t>(f->g->n);
-  if (!sol->m || !sol->status || !sol->chain || !sol->seg || !sol->cached)
+  if (!(sol->m || sol->m32) || !sol->status || !sol->chain || !sol->seg || !sol->cached)
     return fail(RC_E_NOMEM);
   if (hipEventCreate(&sol->ev0) != hipSuccess || hipEventCreate(&sol->ev1) != hipSuccess)
     return fail(RC_E_DEVICE);
-  sol->fill_path = level_only ? 0 : choose_fill_path(f);
+  sol->fill_path = level_only || cell32 ? 0 : choose_fill_path(f);
   if (sol->fill_path != 0 &&
       (hipEventCreate(&sol->evk0) != hipSuccess || hipEventCreate(&sol->evk1) != hipSuccess))
     return fail(RC_E_DEVICE);
@@ -815,6 +825,10 @@ static int solve_one(rc_family f, int64_t B, int32_t objective, void* stream, rc
   rc_solution sol = nullptr;
   const int st0 = new_solution(f, B, objective, &sol, dominance);
   if (st0 != RC_OK) return st0;
+  if (dominance && sol->cell32) {      // the weak-front kernels take 16-bit cells only
+    drop_solution(sol);
+    return RC_E_OVERFLOW;
+  }
   auto fail = [&](int st) {
     (void)hipStreamSynchronize(s);
     drop_solution(sol);
@@ -888,7 +902,22 @@ int rc_solve_batch(rc_family f, const int64_t* B_host, int32_t nb, int32_t objec
   std::vector<BParams> host_prm;
   std::vector<GParams> host_gprm;
   std::vector<WParams> host_wprm;
-  if (s0->fill_path == 3) {
+  // one batched launch when every table takes the same fill (budgets beyond
+  // the 16-bit cells take the level fill, one table at a time)
+  bool same = true;
+  for (rc_solution x : sols) same = same && x->fill_path == s0->fill_path;
+  if (!same) {
+    for (rc_solution x : sols) {
+      const hipError_t fe = x->fill_path == 3   ? launch_fill_wide(x, s)
+                            : x->fill_path == 2 ? launch_fill_ghost(x, s)
+                            : x->fill_path == 1 ? launch_fill_blocked(x, s)
+                                                : launch_fill(x, s);
+      if (fe != hipSuccess) {
+        set_last_error("fill launch", fe);
+        return fail(RC_E_DEVICE);
+      }
+    }
+  } else if (s0->fill_path == 3) {
     host_wprm.resize((size_t)nb);
     WParams* dev_prm = s0->arena.get_n<WParams>(nb);
     if (!dev_prm) return fail(RC_E_NOMEM);
@@ -1010,23 +1039,28 @@ int rc_export_table(rc_solution sol, int64_t first, int64_t count, int64_t* m_ho
     RC_HIP(launch_arg_all(sol, s));
   }
   const int64_t c0 = f->row_off_host[first], c1 = f->row_off_host[first + count];
-  std::vector<uint16_t> mm(c1 - c0), aa(arg_host ? c1 - c0 : 0);
+  std::vector<uint16_t> mm(sol->cell32 ? 0 : c1 - c0), aa(arg_host ? c1 - c0 : 0);
+  std::vector<uint32_t> mm32(sol->cell32 ? c1 - c0 : 0);
   if (c1 > c0) {
-    RC_HIP(hipMemcpyAsync(mm.data(), sol->m + c0, 2 * (c1 - c0), hipMemcpyDeviceToHost, s));
+    if (sol->cell32)
+      RC_HIP(hipMemcpyAsync(mm32.data(), sol->m32 + c0, 4 * (c1 - c0), hipMemcpyDeviceToHost, s));
+    else
+      RC_HIP(hipMemcpyAsync(mm.data(), sol->m + c0, 2 * (c1 - c0), hipMemcpyDeviceToHost, s));
     if (arg_host)
       RC_HIP(hipMemcpyAsync(aa.data(), sol->arg + c0, 2 * (c1 - c0), hipMemcpyDeviceToHost, s));
   }
   RC_HIP(hipStreamSynchronize(s));
+  const uint32_t inf = sol->cell32 ? 0xFFFFFFFFu : kInfM;
   for (int64_t r = 0; r < count; r++) {
     const int64_t set = first + r;
     const int64_t off = f->row_off_host[set] - c0;
     const int64_t w = f->w_host[set];
     for (int64_t t = 0; t < W; t++) {
       const bool in = t < w;
-      const uint32_t mv = in ? mm[off + t] : kInfM;
+      const uint32_t mv = !in ? inf : sol->cell32 ? mm32[off + t] : mm[off + t];
       const uint32_t av = (in && arg_host) ? aa[off + t] : kNoArg;
-      if (m_host) m_host[r * W + t] = mv == kInfM ? -1 : (int64_t)mv;
-      if (arg_host) arg_host[r * W + t] = (mv == kInfM || av == kNoArg) ? -1 : (int32_t)av;
+      if (m_host) m_host[r * W + t] = mv == inf ? -1 : (int64_t)mv;
+      if (arg_host) arg_host[r * W + t] = (mv == inf || av == kNoArg) ? -1 : (int32_t)av;
     }
   }
   return RC_OK;

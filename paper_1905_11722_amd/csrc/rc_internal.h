@@ -35,6 +35,7 @@ constexpr int kMetaInts = 8;                    // blocked fill: int32 per block
 constexpr int kLiveCap = 2048;                  // blocked fill: columns with their own live counts
 constexpr uint32_t kPendM = 0xFFFE;             // blocked fill: cell not written yet
 constexpr int64_t kMaxBudget = 0xFFFC;          // finite opt values stay below kPendM
+constexpr int64_t kMaxBudget32 = (int64_t)1 << 30;   // uint32 cells: min(B, 2 M(V)) up to this
 constexpr int kBlocksFixed = 1;                 // family blocks: kJB targets each (row pushes)
 constexpr int kBlocksGhost = 2;                 // family blocks: cut to fit the ghost halo
 constexpr int kGhostHalo = 64;                  // ghost-zone fill: cells recomputed to the right
@@ -172,6 +173,10 @@ struct rc_family_s {
 };
 
 struct rc_solution_s {
+  // cells of 32 bits when min(B, 2 M(V)) exceeds kMaxBudget: m32 holds the
+  // table (the level fill), m stays null
+  bool cell32 = false;
+  uint32_t* m32 = nullptr;
   rc_family f = nullptr;
   int64_t B = 0, Beff = 0;
   int32_t objective = 0;

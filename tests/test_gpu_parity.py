@@ -125,7 +125,7 @@ def test_empty_and_single(rc, oracle_mod):
         compare(rc, oracle_mod, g1, "pruned", B)
 
 
-def test_budget_clamp_and_overflow(rc, oracle_mod):
+def test_budget_clamp_and_limits(rc, oracle_mod):
     g = W.chain(12, 5)
     gg = rc.Graph.create(g)
     fam = gg.build_family("exact")
@@ -133,20 +133,72 @@ def test_budget_clamp_and_overflow(rc, oracle_mod):
     b = fam.solve(10 ** 9, "tc").table()               # clamped to 2 M(V)
     np.testing.assert_array_equal(a[0], b[0])
     np.testing.assert_array_equal(a[1], b[1])
-    big = W.Graph(2, [[1], []], [3, 4], [40000, 40000])
-    fb = rc.Graph.create(big).build_family("exact")
+    # memory sums the 32-bit cells cannot hold are refused when the graph is made
     with pytest.raises(rc.RcError) as e:
-        fb.solve(10 ** 6, "tc")
-    assert e.value.status == rc.E_OVERFLOW
-    # the largest budget the 16-bit table takes, and one above it
-    small = W.Graph(2, [[1], []], [3, 4], [20000, 20000])
-    compare(rc, oracle_mod, small, "exact", 65532)
-    with pytest.raises(rc.RcError) as e:
-        rc.Graph.create(small).build_family("exact").solve(65533, "tc")
+        rc.Graph.create(W.Graph(2, [[1], []], [3, 4], [1 << 28, 1 << 28]))
     assert e.value.status == rc.E_OVERFLOW
     with pytest.raises(rc.RcError) as e:
         rc.Graph.create(W.antichain(12)).build_family("exact", max_sets=4095)
     assert e.value.status == rc.E_TOO_MANY_SETS
+
+
+# min(B, 2 M(V)) above 65532 does not fit the 16-bit cells: such a table
+# takes 32-bit cells and the level fill.  Both sides of the boundary, and
+# budgets far beyond it.
+@pytest.mark.parametrize("B", [65532, 65533, 80000, 200000, 10 ** 6])
+def test_budgets_beyond_16_bits(rc, oracle_mod, B):
+    small = W.Graph(2, [[1], []], [3, 4], [20000, 20000])     # 2 M(V) = 80000
+    big = W.Graph(2, [[1], []], [3, 4], [40000, 40000])       # 2 M(V) = 160000
+    for g in (small, big):
+        fam = compare(rc, oracle_mod, g, "exact", B)
+        sol = fam.solve(B, "tc")
+        wide = min(B, 2 * sum(g.M)) > 65532
+        assert (sol.fill_kernel() == "k_fill_level") or not wide
+        sol.free()
+
+
+@pytest.mark.parametrize("n,p,seed", RANDOM[::3])
+def test_random_dags_large_memory(rc, oracle_mod, n, p, seed):
+    """Node memories in the tens of thousands: budgets on both sides of the
+    16-bit boundary, both families, both objectives, whole tables."""
+    g = W.random_dag(n, p, 4000 + seed, tmax=40, mmax=30000)
+    lo, hi = 2 * max(g.M), 2 * sum(g.M)
+    for B in sorted({lo, min(65532, hi), 65533, (lo + hi) // 2, hi}):
+        if B < lo:
+            continue
+        for mode in ("exact", "pruned"):
+            compare(rc, oracle_mod, g, mode, B)
+
+
+def test_sweep_across_the_16_bit_boundary(rc, oracle_mod):
+    """A batched sweep whose budgets straddle 65532: tables of both widths
+    in one call, each as its own solve."""
+    g = W.random_dag(9, 0.4, 4242, tmax=40, mmax=30000)
+    lo, hi = 2 * max(g.M), 2 * sum(g.M)
+    assert lo < 65532 < hi
+    budgets = [lo, 65532, 65533, hi]
+    fam = rc.Graph.create(g).build_family("pruned")
+    for B, sol in fam.sweep(budgets, "mc"):
+        ref = oracle_mod.solve(g, "pruned", B, "mc")
+        assert (sol.t_star, sol.m_star) == (ref.t_star, ref.m_star)
+        m, _ = sol.table()
+        np.testing.assert_array_equal(m, ref.table()[0])
+        sol.free()
+
+
+def test_dominance_beyond_16_bits(rc, oracle_mod):
+    """The dominance skip's kernels keep 16-bit cells: a budget beyond them
+    is refused with RC_E_OVERFLOW, one at the boundary is solved."""
+    g = W.random_dag(8, 0.5, 4343, tmax=40, mmax=30000)
+    B = 2 * sum(g.M)
+    assert B > 65532
+    fam = rc.Graph.create(g).build_family("exact")
+    with pytest.raises(rc.RcError) as e:
+        fam.solve_dominance(B)
+    assert e.value.status == rc.E_OVERFLOW
+    d = fam.solve_dominance(65532)
+    ref = oracle_mod.solve(g, "exact", 65532, "tc")
+    assert (d.t_star, d.m_star) == (ref.t_star, ref.m_star)
 
 
 def test_largest_exact_family(rc, oracle_mod):
