@@ -7,7 +7,10 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <memory>
+#include <mutex>
 #include <new>
+#include <utility>
 #include <vector>
 
 #include "rc_internal.h"
@@ -35,6 +38,52 @@ void set_last_error(const char* what, hipError_t e) {
 
 void set_last_error_msg(const char* msg) {
   std::snprintf(g_last_error, sizeof(g_last_error), "%s", msg);
+}
+
+namespace {
+// Free pinned buffers, smallest first: a request takes the smallest that
+// fits, or allocates a power of two of at least 64 KB.  Never destroyed, so
+// that no buffer is released after the runtime has shut down.
+struct StagingPool {
+  std::mutex mu;
+  std::vector<std::pair<size_t, char*>> free_list;
+};
+StagingPool& staging_pool() {
+  static StagingPool* pool = new StagingPool();
+  return *pool;
+}
+}  // namespace
+
+Staging::Staging(size_t bytes) {
+  StagingPool& pool = staging_pool();
+  {
+    std::lock_guard<std::mutex> lock(pool.mu);
+    auto& fl = pool.free_list;
+    for (size_t x = 0; x < fl.size(); x++) {
+      if (fl[x].first >= bytes) {
+        n_ = fl[x].first;
+        p_ = fl[x].second;
+        fl.erase(fl.begin() + (std::ptrdiff_t)x);
+        return;
+      }
+    }
+  }
+  size_t n = (size_t)64 << 10;
+  while (n < bytes) n <<= 1;
+  void* p = nullptr;
+  if (hipHostMalloc(&p, n, hipHostMallocDefault) != hipSuccess) return;
+  p_ = static_cast<char*>(p);
+  n_ = n;
+}
+
+Staging::~Staging() {
+  if (!p_ || pending_) return;
+  StagingPool& pool = staging_pool();
+  std::lock_guard<std::mutex> lock(pool.mu);
+  auto& fl = pool.free_list;
+  auto it = fl.begin();
+  while (it != fl.end() && it->first < n_) ++it;
+  fl.insert(it, {n_, p_});
 }
 
 // Sizes of the memory-indexed table of one solve (rc_solve_dual): argument
@@ -261,6 +310,7 @@ int rc_graph_create(int32_t n, const int32_t* row_ptr, const int32_t* col_idx, c
   g->arena.free_fn = free_fn;
   g->arena.user = user;
   g->num_depths = D;
+  for (int v = 0; v < n; v++) g->num_sinks += succs[v].empty() ? 1 : 0;
   hipStream_t s = as_stream(stream);
   int st = RC_OK;
   int32_t *d_row_ptr = nullptr, *d_col_idx = nullptr;
@@ -339,10 +389,12 @@ static void cut_blocks(rc_family f, const std::vector<int32_t>& near_h) {
   f->bstart_host.push_back((int32_t)f->F);
 }
 
-// Block starts to the device, then the number of panel sources per block
-// and their offsets (rec_ptr).  Uses the family arena; counts is scratch of
-// at least nblk + 1 entries.
-static int upload_blocks(rc_family f, int64_t* counts, hipStream_t s) {
+// Block starts to the device (through pinned memory), then the number of
+// panel sources per block and their offsets (rec_ptr).  Uses the family
+// arena; counts is scratch of at least nblk + 1 entries.  The staging
+// buffer must stay alive until the stream has been synchronised.
+static int upload_blocks(rc_family f, int64_t* counts, std::unique_ptr<Staging>& stage,
+                         hipStream_t s) {
   Arena& A = f->arena;
   f->nblk = (int64_t)f->bstart_host.size() - 1;
   if (f->nblk <= 0) {
@@ -352,13 +404,30 @@ static int upload_blocks(rc_family f, int64_t* counts, hipStream_t s) {
   f->bstart = A.get_n<int32_t>(f->nblk + 1);
   f->rec_ptr = A.get_n<int64_t>(f->nblk + 1);
   if (!f->bstart || !f->rec_ptr) return RC_E_NOMEM;
-  if (hipMemcpyAsync(f->bstart, f->bstart_host.data(), sizeof(int32_t) * (size_t)(f->nblk + 1),
-                     hipMemcpyHostToDevice, s) != hipSuccess ||
+  const size_t bytes = sizeof(int32_t) * (size_t)(f->nblk + 1);
+  stage.reset(new (std::nothrow) Staging(bytes));
+  if (!stage || !stage->data()) return RC_E_NOMEM;
+  std::memcpy(stage->data(), f->bstart_host.data(), bytes);
+  stage->in_flight();
+  if (hipMemcpyAsync(f->bstart, stage->data(), bytes, hipMemcpyHostToDevice, s) != hipSuccess ||
       launch_blk_count(f, f->nblk, counts, s) != hipSuccess ||
       launch_scan(counts, f->rec_ptr, f->nblk, 1, s) != hipSuccess)
     return RC_E_DEVICE;
   return RC_OK;
 }
+
+// Sets of the pruned family: the n ancestor sets L^v (distinct, since v is
+// the one maximal node of L^v), the empty set, and V unless V is one of the
+// L^v, which happens exactly when the graph has a single sink (every node
+// then reaches it).
+static int64_t pruned_family_size(rc_graph g) {
+  if (g->n == 0) return 1;
+  return (int64_t)g->n + 1 + (g->num_sinks > 1 ? 1 : 0);
+}
+
+// Record buffers up to this many records are sized from an upper bound
+// (every record holds at least one pair) without waiting for their count.
+constexpr int64_t kRecordBound = (int64_t)1 << 18;
 
 static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
   rc_graph g = f->g;
@@ -368,6 +437,7 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
   tmp.alloc = A.alloc;
   tmp.free_fn = A.free_fn;
   tmp.user = A.user;
+  std::unique_ptr<Staging> up_stage;  // host -> device block starts
   struct TmpGuard {
     Arena& a;
     hipStream_t s;
@@ -376,30 +446,52 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
       a.release_all();
     }
   } guard{tmp, s};
+  // Host -> device and device -> host copies go through pinned buffers; a
+  // build waits for the stream once for the family's size (exact family
+  // only), once for its shape and pair count, once more for the near shifts
+  // of a ghost-zone family, and once at the end.
+  auto sync_landed = [&](Staging& st) -> int {
+    if (hipStreamSynchronize(s) != hipSuccess) {
+      set_last_error_msg("family build: stream synchronisation failed");
+      return RC_E_DEVICE;
+    }
+    st.landed();
+    return RC_OK;
+  };
 
   f->status = A.get_n<DevStatus>(1);
   if (!f->status) return RC_E_NOMEM;
   RC_HIP(launch_zero(f->status, sizeof(DevStatus), s));
 
   // ---- a2: the family as bitmasks, in canonical order
-  const int64_t cap = f->mode == RC_FAMILY_PRUNED ? (int64_t)n + 2 : max_sets;
+  const bool pruned = f->mode == RC_FAMILY_PRUNED;
+  const int64_t cap = pruned ? (int64_t)n + 2 : max_sets;
   f->fstride = cap;
   uint64_t* cand = tmp.get_n<uint64_t>(cap * words);
   int32_t* lvl = tmp.get_n<int32_t>(n + 3);
   f->bits = A.get_n<uint64_t>(cap * words);
   if (!cand || !lvl || !f->bits) return RC_E_NOMEM;
-  if (f->mode == RC_FAMILY_PRUNED) {
+  if (pruned) {
     RC_HIP(launch_pruned_candidates(g, g->dAnc, cand, s));
   } else {
     RC_HIP(launch_enum_exact(g, cand, cap, lvl, f->status, s));
   }
   RC_HIP(launch_rank(g, f->mode, cand, cap, lvl, f->bits, f->fstride, f->status, s));
-  DevStatus hs;
-  RC_HIP(hipMemcpyAsync(&hs, f->status, sizeof(hs), hipMemcpyDeviceToHost, s));
-  RC_HIP(hipStreamSynchronize(s));
-  if (hs.overflow) return RC_E_TOO_MANY_SETS;
-  if (hs.error) return RC_E_DEVICE;
-  const int64_t F = hs.count;
+  int64_t F = 0;
+  if (pruned) {
+    F = pruned_family_size(g);          // checked against the device's count below
+  } else {
+    Staging st0(sizeof(DevStatus));
+    if (!st0.data()) return RC_E_NOMEM;
+    st0.in_flight();
+    RC_HIP(hipMemcpyAsync(st0.data(), f->status, sizeof(DevStatus), hipMemcpyDeviceToHost, s));
+    const int ss = sync_landed(st0);
+    if (ss != RC_OK) return ss;
+    const DevStatus& h0 = *st0.at<DevStatus>(0);
+    if (h0.overflow) return RC_E_TOO_MANY_SETS;
+    if (h0.error) return RC_E_DEVICE;
+    F = h0.count;
+  }
   if (F < 1 || F > max_sets) return RC_E_TOO_MANY_SETS;
   f->F = F;
 
@@ -425,15 +517,73 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
   RC_HIP(launch_row_widths(f, padded, s));
   RC_HIP(launch_scan(padded, f->row_off, F, 1, s));
   RC_HIP(launch_row_align(f, s));
-
-  // ---- a4: predecessor pairs
+  // ---- a4: predecessor pairs, counted per target
   RC_HIP(launch_pair_count(f, counts, s));
   RC_HIP(launch_scan(counts, f->pred_ptr, F, 1, s));
-  int64_t P = 0;
-  RC_HIP(hipMemcpyAsync(&P, f->pred_ptr + F, sizeof(P), hipMemcpyDeviceToHost, s));
-  RC_HIP(hipStreamSynchronize(s));
-  if (P < 0 || P >= ((int64_t)1 << 40)) return RC_E_OVERFLOW;
-  f->P = P;
+
+  // ---- the family's shape to the host: sizes, widths, row offsets, pairs
+  StageLayout L1;
+  const size_t o_st = L1.add<DevStatus>(1), o_size = L1.add<int32_t>(F),
+               o_w = L1.add<int32_t>(F), o_off = L1.add<int64_t>(F + 1),
+               o_pp = L1.add<int64_t>(F + 1);
+  {
+    Staging st1(L1.bytes);
+    if (!st1.data()) return RC_E_NOMEM;
+    st1.in_flight();
+    RC_HIP(hipMemcpyAsync(st1.at<char>(o_st), f->status, sizeof(DevStatus),
+                          hipMemcpyDeviceToHost, s));
+    RC_HIP(hipMemcpyAsync(st1.at<char>(o_size), f->size, sizeof(int32_t) * F,
+                          hipMemcpyDeviceToHost, s));
+    RC_HIP(hipMemcpyAsync(st1.at<char>(o_w), f->w, sizeof(int32_t) * F, hipMemcpyDeviceToHost, s));
+    RC_HIP(hipMemcpyAsync(st1.at<char>(o_off), f->row_off, sizeof(int64_t) * (F + 1),
+                          hipMemcpyDeviceToHost, s));
+    RC_HIP(hipMemcpyAsync(st1.at<char>(o_pp), f->pred_ptr, sizeof(int64_t) * (F + 1),
+                          hipMemcpyDeviceToHost, s));
+    const int ss = sync_landed(st1);
+    if (ss != RC_OK) return ss;
+    const DevStatus& h1 = *st1.at<DevStatus>(o_st);
+    if (h1.overflow) return RC_E_TOO_MANY_SETS;
+    if (h1.error) return RC_E_DEVICE;
+    if (h1.count != F) {
+      set_last_error_msg("family build: the device counted another family size");
+      return RC_E_DEVICE;
+    }
+    const int32_t* size_h = st1.at<int32_t>(o_size);
+    const int32_t* w_h = st1.at<int32_t>(o_w);
+    const int64_t* off_h = st1.at<int64_t>(o_off);
+    const int64_t* pp_h = st1.at<int64_t>(o_pp);
+    f->w_host.assign(w_h, w_h + F);
+    f->row_off_host.assign(off_h, off_h + F + 1);
+    f->cells = off_h[F];
+    f->cells_alloc = f->cells + kGuard;
+    f->P = pp_h[F];
+    if (f->P < 0 || f->P >= ((int64_t)1 << 40) || f->cells >= ((int64_t)1 << 40))
+      return RC_E_OVERFLOW;
+    f->level_ptr.clear();
+    f->level_maxw.clear();
+    f->max_row = 0;
+    for (int64_t i = 0; i < F; i++) {
+      if (i == 0 || size_h[i] != size_h[i - 1]) {
+        f->level_ptr.push_back(i);
+        f->level_maxw.push_back(0);
+      }
+      f->level_maxw.back() = std::max(f->level_maxw.back(), w_h[i]);
+      f->max_row = std::max<int64_t>(f->max_row, w_h[i]);
+    }
+    f->level_ptr.push_back(F);
+    // the most pairs of a target per size level (the memory-indexed table
+    // runs that many pairs per level launch)
+    f->level_pairs.clear();
+    for (size_t l = 0; l + 1 < f->level_ptr.size(); l++) {
+      int64_t most = 0;
+      for (int64_t j = f->level_ptr[l]; j < f->level_ptr[l + 1]; j++)
+        most = std::max(most, pp_h[j + 1] - pp_h[j]);
+      f->level_pairs.push_back(most);
+    }
+  }
+
+  // ---- a4: the pairs themselves and the relaxation count
+  const int64_t P = f->P;
   f->pidx = A.get_n<int32_t>(P);
   f->pdt = A.get_n<int32_t>(P);
   f->pdm = A.get_n<int32_t>(P);
@@ -441,84 +591,50 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
   if (!f->pidx || !f->pdt || !f->pdm || !f->pc) return RC_E_NOMEM;
   RC_HIP(launch_pair_write(f, walg_t, s));
   RC_HIP(launch_sum(walg_t, F, &f->status->walg, s));
-  // blocks of the wavefront fills: kJB targets each for the row-push fill;
-  // for the ghost-zone fill cut on the host from the shifts of near pairs
-  f->blk_kind = family_block_kind(f, false);
-  std::vector<int32_t> near_h;
-  int32_t* near_d = nullptr;
-  if (f->blk_kind != 0 && f->blk_kind != kBlocksFixed) {
-    near_h.resize((size_t)(F * kNear));
-    near_d = tmp.get_n<int32_t>(F * kNear);
+
+  // ---- blocks of the wavefront fills: kJB targets each for the row-push
+  // fill; for the ghost-zone fill cut on the host from the shifts of near
+  // pairs
+  f->blk_kind = family_block_kind(f, true);
+  if (f->blk_kind == kBlocksGhost) {
+    int32_t* near_d = tmp.get_n<int32_t>(F * kNear);
     if (!near_d) return RC_E_NOMEM;
     RC_HIP(launch_near_shifts(f, near_d, s));
+    Staging st2(sizeof(int32_t) * (size_t)(F * kNear));
+    if (!st2.data()) return RC_E_NOMEM;
+    st2.in_flight();
+    RC_HIP(hipMemcpyAsync(st2.data(), near_d, sizeof(int32_t) * (size_t)(F * kNear),
+                          hipMemcpyDeviceToHost, s));
+    const int ss = sync_landed(st2);
+    if (ss != RC_OK) return ss;
+    const int32_t* nh = st2.at<int32_t>(0);
+    cut_blocks(f, std::vector<int32_t>(nh, nh + F * kNear));
+  } else if (f->blk_kind == kBlocksFixed) {
+    cut_blocks(f, std::vector<int32_t>());
   }
-  if (f->blk_kind == kBlocksFixed) {
-    cut_blocks(f, near_h);
-    const int ub = upload_blocks(f, counts, s);
+  if (f->blk_kind != 0) {
+    const int ub = upload_blocks(f, counts, up_stage, s);
     if (ub != RC_OK) return ub;
   }
 
-  // ---- host copies for launch configuration
-  std::vector<int32_t> size_h(F);
-  f->w_host.resize(F);
-  f->row_off_host.resize(F + 1);
-  RC_HIP(hipMemcpyAsync(size_h.data(), f->size, sizeof(int32_t) * F, hipMemcpyDeviceToHost, s));
-  RC_HIP(hipMemcpyAsync(f->w_host.data(), f->w, sizeof(int32_t) * F, hipMemcpyDeviceToHost, s));
-  RC_HIP(hipMemcpyAsync(f->row_off_host.data(), f->row_off, sizeof(int64_t) * (F + 1),
-                        hipMemcpyDeviceToHost, s));
-  std::vector<int64_t> pred_ptr_h(F + 1);
-  RC_HIP(hipMemcpyAsync(pred_ptr_h.data(), f->pred_ptr, sizeof(int64_t) * (F + 1),
-                        hipMemcpyDeviceToHost, s));
-  RC_HIP(hipMemcpyAsync(&hs, f->status, sizeof(hs), hipMemcpyDeviceToHost, s));
+  // ---- panel records: buffers sized from the bound P when it is small,
+  // else from the count (one more wait)
   f->rec_total = 0;
-  if (f->nblk > 0)
-    RC_HIP(hipMemcpyAsync(&f->rec_total, f->rec_ptr + f->nblk, sizeof(int64_t),
+  int64_t rec_cap = std::min<int64_t>(P, f->nblk * F);
+  if (f->nblk > 0 && rec_cap > kRecordBound) {
+    Staging st3(sizeof(int64_t));
+    if (!st3.data()) return RC_E_NOMEM;
+    st3.in_flight();
+    RC_HIP(hipMemcpyAsync(st3.data(), f->rec_ptr + f->nblk, sizeof(int64_t),
                           hipMemcpyDeviceToHost, s));
-  if (near_d)
-    RC_HIP(hipMemcpyAsync(near_h.data(), near_d, sizeof(int32_t) * near_h.size(),
-                          hipMemcpyDeviceToHost, s));
-  RC_HIP(hipStreamSynchronize(s));
-  if (hs.error) return RC_E_DEVICE;
-  f->cells = f->row_off_host[F];
-  f->cells_alloc = f->cells + kGuard;
-  if (f->cells >= ((int64_t)1 << 40)) return RC_E_OVERFLOW;
-  f->level_ptr.clear();
-  f->level_maxw.clear();
-  f->max_row = 0;
-  for (int64_t i = 0; i < F; i++) {
-    if (i == 0 || size_h[i] != size_h[i - 1]) {
-      f->level_ptr.push_back(i);
-      f->level_maxw.push_back(0);
-    }
-    f->level_maxw.back() = std::max(f->level_maxw.back(), f->w_host[i]);
-    f->max_row = std::max<int64_t>(f->max_row, f->w_host[i]);
+    const int ss = sync_landed(st3);
+    if (ss != RC_OK) return ss;
+    rec_cap = *st3.at<int64_t>(0);
   }
-  f->level_ptr.push_back(F);
-  // the most pairs of a target per size level (the memory-indexed table
-  // runs that many pairs per level launch)
-  f->level_pairs.clear();
-  for (size_t l = 0; l + 1 < f->level_ptr.size(); l++) {
-    int64_t most = 0;
-    for (int64_t j = f->level_ptr[l]; j < f->level_ptr[l + 1]; j++)
-      most = std::max(most, pred_ptr_h[j + 1] - pred_ptr_h[j]);
-    f->level_pairs.push_back(most);
-  }
-  if (near_d) {                                // kind not fixed before the host copies
-    if (f->blk_kind < 0) f->blk_kind = family_block_kind(f, true);
-    cut_blocks(f, near_h);
-    const int ub = upload_blocks(f, counts, s);
-    if (ub != RC_OK) return ub;
-    if (f->nblk > 0) {
-      RC_HIP(hipMemcpyAsync(&f->rec_total, f->rec_ptr + f->nblk, sizeof(int64_t),
-                            hipMemcpyDeviceToHost, s));
-      RC_HIP(hipStreamSynchronize(s));
-    }
-  }
-  f->relax = hs.walg;
-  f->has_records = false;
-  if (f->nblk > 0 && f->rec_total <= kMaxRecords) {
+  const bool records = f->nblk > 0 && rec_cap <= kMaxRecords;
+  if (records) {
     BlockRecords& R = f->rec;
-    const int64_t Rn = f->rec_total, T3 = f->nblk * kJB * kJB;
+    const int64_t Rn = rec_cap, T3 = f->nblk * kJB * kJB;
     R.src = A.get_n<int32_t>(Rn);
     R.e = A.get_n<int32_t>(Rn * kJB);
     R.kadd = A.get_n<uint32_t>(Rn * kJB);
@@ -533,28 +649,57 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
     if (!f->clu_ptr) return RC_E_NOMEM;
     RC_HIP(launch_blk_clusters(f, counts, s));
     RC_HIP(launch_scan(counts, f->clu_ptr, f->nblk, 1, s));
-    RC_HIP(hipMemcpyAsync(&f->clu_total, f->clu_ptr + f->nblk, sizeof(int64_t),
-                          hipMemcpyDeviceToHost, s));
-    // the split-panel fill: one record per (block, source, shift), a block's
-    // records sorted in LDS, byte offsets of the table in 31 bits
-    std::vector<int64_t> wcount;
-    if (f->blk_kind == kBlocksFixed) {
-      f->wrec_ptr = A.get_n<int64_t>(f->nblk + 1);
-      if (!f->wrec_ptr) return RC_E_NOMEM;
-      RC_HIP(launch_wide_count(f, counts, s));
-      wcount.resize((size_t)f->nblk);
-      RC_HIP(hipMemcpyAsync(wcount.data(), counts, sizeof(int64_t) * (size_t)f->nblk,
-                            hipMemcpyDeviceToHost, s));
-      RC_HIP(launch_scan(counts, f->wrec_ptr, f->nblk, 1, s));
-      RC_HIP(hipMemcpyAsync(&f->wrec_total, f->wrec_ptr + f->nblk, sizeof(int64_t),
-                            hipMemcpyDeviceToHost, s));
-    }
-    RC_HIP(hipStreamSynchronize(s));
-    f->has_records = true;
-    f->has_wide = f->blk_kind == kBlocksFixed && 2 * f->cells_alloc < INT32_MAX &&
-                  f->wrec_total < ((int64_t)1 << 26);
-    for (int64_t x : wcount) f->has_wide = f->has_wide && x <= kWMaxRec;
   }
+  // the split-panel fill: one record per (block, source, shift), a block's
+  // records sorted in LDS, byte offsets of the table in 31 bits
+  int64_t* wcounts = nullptr;
+  if (records && f->blk_kind == kBlocksFixed) {
+    f->wrec_ptr = A.get_n<int64_t>(f->nblk + 1);
+    wcounts = tmp.get_n<int64_t>(f->nblk + 1);
+    if (!f->wrec_ptr || !wcounts) return RC_E_NOMEM;
+    RC_HIP(launch_wide_count(f, wcounts, s));
+    RC_HIP(launch_scan(wcounts, f->wrec_ptr, f->nblk, 1, s));
+  }
+
+  // ---- the counts to the host: status (relaxations, errors), records
+  StageLayout L4;
+  const size_t q_st = L4.add<DevStatus>(1), q_rec = L4.add<int64_t>(1),
+               q_clu = L4.add<int64_t>(1), q_wrec = L4.add<int64_t>(1),
+               q_wc = L4.add<int64_t>(wcounts ? f->nblk : 0);
+  Staging st4(L4.bytes);
+  if (!st4.data()) return RC_E_NOMEM;
+  st4.in_flight();
+  RC_HIP(hipMemcpyAsync(st4.at<char>(q_st), f->status, sizeof(DevStatus), hipMemcpyDeviceToHost,
+                        s));
+  if (f->nblk > 0)
+    RC_HIP(hipMemcpyAsync(st4.at<char>(q_rec), f->rec_ptr + f->nblk, sizeof(int64_t),
+                          hipMemcpyDeviceToHost, s));
+  if (records)
+    RC_HIP(hipMemcpyAsync(st4.at<char>(q_clu), f->clu_ptr + f->nblk, sizeof(int64_t),
+                          hipMemcpyDeviceToHost, s));
+  if (wcounts) {
+    RC_HIP(hipMemcpyAsync(st4.at<char>(q_wrec), f->wrec_ptr + f->nblk, sizeof(int64_t),
+                          hipMemcpyDeviceToHost, s));
+    RC_HIP(hipMemcpyAsync(st4.at<char>(q_wc), wcounts, sizeof(int64_t) * (size_t)f->nblk,
+                          hipMemcpyDeviceToHost, s));
+  }
+  const int ss = sync_landed(st4);
+  if (ss != RC_OK) return ss;
+  if (up_stage) up_stage->landed();
+  const DevStatus& h4 = *st4.at<DevStatus>(q_st);
+  if (h4.error) return RC_E_DEVICE;
+  f->relax = h4.walg;
+  f->rec_total = f->nblk > 0 ? *st4.at<int64_t>(q_rec) : 0;
+  if (f->rec_total > rec_cap) {
+    set_last_error_msg("family build: more panel records than pairs");
+    return RC_E_DEVICE;
+  }
+  f->has_records = records;
+  f->clu_total = records ? *st4.at<int64_t>(q_clu) : 0;
+  f->wrec_total = wcounts ? *st4.at<int64_t>(q_wrec) : 0;
+  f->has_wide = wcounts && 2 * f->cells_alloc < INT32_MAX && f->wrec_total < ((int64_t)1 << 26);
+  for (int64_t b = 0; wcounts && b < f->nblk; b++)
+    f->has_wide = f->has_wide && st4.at<int64_t>(q_wc)[b] <= kWMaxRec;
   return RC_OK;
 }
 
@@ -853,10 +998,15 @@ static int solve_one(rc_family f, int64_t B, int32_t objective, void* stream, rc
   }
   if (hipEventRecord(sol->ev1, s) != hipSuccess) return fail(RC_E_DEVICE);
   if (launch_select(sol, s) != hipSuccess) return fail(RC_E_DEVICE);
-  DevStatus hs;
-  if (hipMemcpyAsync(&hs, sol->status, sizeof(hs), hipMemcpyDeviceToHost, s) != hipSuccess ||
+  Staging stage(sizeof(DevStatus));
+  if (!stage.data()) return fail(RC_E_NOMEM);
+  stage.in_flight();
+  if (hipMemcpyAsync(stage.data(), sol->status, sizeof(DevStatus), hipMemcpyDeviceToHost, s) !=
+          hipSuccess ||
       hipStreamSynchronize(s) != hipSuccess)
     return fail(RC_E_DEVICE);
+  stage.landed();
+  const DevStatus hs = *stage.at<DevStatus>(0);
   const float fill_ms = elapsed(sol->ev0, sol->ev1);
   const float kernel_ms = sol->evk0 ? elapsed(sol->evk0, sol->evk1) : fill_ms;
   const int st = settle_solution(sol, hs, fill_ms, kernel_ms);
@@ -956,16 +1106,19 @@ int rc_solve_batch(rc_family f, const int64_t* B_host, int32_t nb, int32_t objec
   if (hipEventRecord(s0->ev1, s) != hipSuccess) return fail(RC_E_DEVICE);
   for (rc_solution x : sols)
     if (launch_select(x, s) != hipSuccess) return fail(RC_E_DEVICE);
-  std::vector<DevStatus> hs((size_t)nb);
+  Staging stage(sizeof(DevStatus) * (size_t)nb);
+  if (!stage.data()) return fail(RC_E_NOMEM);
+  stage.in_flight();
   for (int32_t b = 0; b < nb; b++)
-    if (hipMemcpyAsync(&hs[b], sols[b]->status, sizeof(DevStatus), hipMemcpyDeviceToHost, s) !=
-        hipSuccess)
+    if (hipMemcpyAsync(stage.at<DevStatus>(0) + b, sols[b]->status, sizeof(DevStatus),
+                       hipMemcpyDeviceToHost, s) != hipSuccess)
       return fail(RC_E_DEVICE);
   if (hipStreamSynchronize(s) != hipSuccess) return fail(RC_E_DEVICE);
+  stage.landed();
   const float fill_ms = elapsed(s0->ev0, s0->ev1);
   const float kernel_ms = s0->evk0 ? elapsed(s0->evk0, s0->evk1) : fill_ms;
   for (int32_t b = 0; b < nb; b++) {
-    const int st = settle_solution(sols[b], hs[b], fill_ms, kernel_ms);
+    const int st = settle_solution(sols[b], stage.at<DevStatus>(0)[b], fill_ms, kernel_ms);
     if (st < 0) return fail(st);
   }
   for (int32_t b = 0; b < nb; b++) {
@@ -1002,25 +1155,36 @@ int rc_reconstruct(rc_solution sol, void* stream, int32_t* k, int32_t* chain_hos
   hipStream_t s = as_stream(stream);
   rc_family f = sol->f;
   const int n = f->g->n;
+  // the chain has at most min(F, n + 1) sets: every step adds a node
+  const int64_t kmax = std::min<int64_t>(f->F, (int64_t)n + 1);
+  StageLayout lay;
+  const size_t o_st = lay.add<DevStatus>(1), o_ch = lay.add<int32_t>(kmax),
+               o_sg = lay.add<int32_t>(n), o_ca = lay.add<uint8_t>(n);
+  Staging stage(lay.bytes);
+  if (!stage.data()) return RC_E_NOMEM;
   RC_HIP(launch_trace(sol, s));
-  DevStatus hs;
-  RC_HIP(hipMemcpyAsync(&hs, sol->status, sizeof(hs), hipMemcpyDeviceToHost, s));
-  std::vector<int32_t> ch(f->F), sg(n);
-  std::vector<uint8_t> ca(n);
-  RC_HIP(hipMemcpyAsync(ch.data(), sol->chain, sizeof(int32_t) * f->F, hipMemcpyDeviceToHost, s));
+  stage.in_flight();
+  RC_HIP(hipMemcpyAsync(stage.at<char>(o_st), sol->status, sizeof(DevStatus),
+                        hipMemcpyDeviceToHost, s));
+  if (kmax > 0)
+    RC_HIP(hipMemcpyAsync(stage.at<char>(o_ch), sol->chain, sizeof(int32_t) * (size_t)kmax,
+                          hipMemcpyDeviceToHost, s));
   if (n > 0) {
-    RC_HIP(hipMemcpyAsync(sg.data(), sol->seg, sizeof(int32_t) * n, hipMemcpyDeviceToHost, s));
-    RC_HIP(hipMemcpyAsync(ca.data(), sol->cached, n, hipMemcpyDeviceToHost, s));
+    RC_HIP(hipMemcpyAsync(stage.at<char>(o_sg), sol->seg, sizeof(int32_t) * n,
+                          hipMemcpyDeviceToHost, s));
+    RC_HIP(hipMemcpyAsync(stage.at<char>(o_ca), sol->cached, n, hipMemcpyDeviceToHost, s));
   }
   RC_HIP(hipStreamSynchronize(s));
-  if (hs.error || hs.k < 0 || hs.k > f->F) {
+  stage.landed();
+  const DevStatus hs = *stage.at<DevStatus>(o_st);
+  if (hs.error || hs.k < 0 || hs.k > kmax) {
     set_last_error_msg("traceback: optarg walk did not end at (empty set, 0)");
     return RC_E_DEVICE;
   }
   if (k) *k = hs.k;
-  if (chain_host) std::copy(ch.begin(), ch.begin() + hs.k, chain_host);
-  if (seg_host) std::copy(sg.begin(), sg.end(), seg_host);
-  if (cached_host) std::copy(ca.begin(), ca.end(), cached_host);
+  if (chain_host) std::copy(stage.at<int32_t>(o_ch), stage.at<int32_t>(o_ch) + hs.k, chain_host);
+  if (seg_host) std::copy(stage.at<int32_t>(o_sg), stage.at<int32_t>(o_sg) + n, seg_host);
+  if (cached_host) std::copy(stage.at<uint8_t>(o_ca), stage.at<uint8_t>(o_ca) + n, cached_host);
   if (overhead) *overhead = hs.overhead;
   if (peak) *peak = hs.peak;
   if (cache_mem) *cache_mem = hs.cache_mem;

@@ -127,6 +127,7 @@ struct rc_graph_s {
   int32_t* dByDepth = nullptr;    // nodes sorted by depth (longest path from a source)
   int32_t* dDepthPtr = nullptr;   // [num_depths+1]
   int32_t num_depths = 0;
+  int32_t num_sinks = 0;          // nodes without successors
   uint64_t* dAnc = nullptr;       // [n][words] ancestors of each node (without the node),
                                   // the pruned family's generators, computed once per graph
 };
@@ -221,6 +222,44 @@ namespace rcdp {
 // Thread-local description of the last RC_E_DEVICE (rc_api.hip).
 void set_last_error(const char* what, hipError_t e);
 void set_last_error_msg(const char* msg);
+
+// Pinned host memory for the copies between host and device inside one
+// call (rc_api.hip).  A copy to or from pinned memory is asynchronous, so
+// the copies of a call cost one synchronisation of the stream; a copy to or
+// from pageable memory waits for itself.  Buffers come from a process-wide
+// pool (kept until the process ends), one caller at a time; data() is null
+// when pinned memory could not be had.  Between in_flight() (copies are
+// enqueued) and landed() (the stream was synchronised) the buffer is not
+// returned to the pool: a call that leaves on an error in between gives it
+// up rather than hand a buffer with copies still pending to another call.
+class Staging {
+ public:
+  explicit Staging(size_t bytes);
+  ~Staging();
+  Staging(const Staging&) = delete;
+  Staging& operator=(const Staging&) = delete;
+  char* data() const { return p_; }
+  template <class T> T* at(size_t byte_offset) const {
+    return reinterpret_cast<T*>(p_ + byte_offset);
+  }
+  void in_flight() { pending_ = true; }
+  void landed() { pending_ = false; }
+
+ private:
+  char* p_ = nullptr;
+  size_t n_ = 0;
+  bool pending_ = false;
+};
+
+// Byte offsets of consecutive parts of a staging buffer, each aligned to 64.
+struct StageLayout {
+  size_t bytes = 0;
+  template <class T> size_t add(int64_t count) {
+    const size_t off = bytes;
+    bytes += (sizeof(T) * (size_t)(count > 0 ? count : 0) + 63) & ~size_t(63);
+    return off;
+  }
+};
 
 // ---- utilities (family.hip)
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);  // bytes % 8 == 0
