@@ -42,7 +42,8 @@
  * none changes a result, only which kernels compute it and how they are
  * shaped; an unrecognised value is ignored):
  *  - RCDP_FILL = level | wavefront | wide | ghost: the fill of Algorithm 1.
- *    level: one launch per group of equal-size sets (k_fill_level).
+ *    level: one launch per group of equal-size sets (k_fill_level_vec on
+ *    16-bit cells, k_fill_level on 32-bit cells).
  *    wavefront: the persistent row-push wavefront over fixed blocks of
  *    targets (k_fill_blocked).  wide: the split-panel wavefront over fixed
  *    blocks (k_fill_wide).  ghost: the wavefront over ghost-zone blocks
@@ -283,9 +284,10 @@ int rc_solution_fill_ms(rc_solution s, float* ms);
 int rc_solution_fill_kernel_ms(rc_solution s, float* ms);
 /* Which fill the solve ran (all of them compute the same table, Algorithm 1
  * of Section 4.2): *path = 0 one launch per group of equal-size sets
- * (k_fill_level), 1 the persistent row-push wavefront (k_fill_blocked), 2
- * the ghost-zone wavefront (k_fill_ghost), 3 the split-panel wavefront
- * (k_fill_wide).  Returns RC_OK or RC_E_ARG (NULL argument). */
+ * (k_fill_level_vec / k_fill_level), 1 the persistent row-push wavefront
+ * (k_fill_blocked), 2 the ghost-zone wavefront (k_fill_ghost), 3 the
+ * split-panel wavefront (k_fill_wide).  Returns RC_OK or RC_E_ARG (NULL
+ * argument). */
 int rc_solution_fill_path(rc_solution s, int32_t* path);
 
 /*

@@ -27,6 +27,7 @@
 #include "rc_internal.h"
 #include "dominance.h"
 #include "schedule.h"
+#include "wavefront.h"
 
 namespace rcdp {
 
@@ -115,6 +116,93 @@ __global__ __launch_bounds__(kFillThreads) void k_fill_level(
     const int32_t tp = tile0 + r * kFillThreads + (int32_t)threadIdx.x;
     if (tp < wj) mo[tp] = (T)acc[r];
   }
+}
+
+// The level fill for 16-bit cells, eight cells per thread, two per packed
+// instruction.  Cells are counted from the row's end, which lies on a
+// kRowAlign boundary: thread group g of target j owns the cells at
+// [E_j - 8 (g + 1), E_j - 8 g) (E_j = end of the row), one aligned 16-byte
+// store, and the source cell of target cell x along a pair is x + D with
+// D = row_off[i] - row_off[j] - dt, the same for every cell of the pair.
+// So a pair's eight source cells start D mod 8 cells past an aligned
+// 16-byte word: two aligned loads and a shift by that uniform amount.
+// Source cells outside [0, ws[i]) and target cells before the row's first
+// cell read as infinity.  ws as for k_fill_level.
+constexpr int kVecCells = 8;
+constexpr int kVecTile = kFillThreads * kVecCells;
+
+// words w[0..7] hold cells 0..15 of two aligned 16-byte loads; out[q] gets
+// cells a + 2q and a + 2q + 1 (a uniform, 0..7)
+template <int a>
+__device__ __forceinline__ void take8(const uint32_t (&w)[8], uint32_t (&out)[4]) {
+#pragma unroll
+  for (int q = 0; q < 4; q++) {
+    if (a % 2 == 0)
+      out[q] = w[a / 2 + q];
+    else
+      out[q] = __builtin_amdgcn_alignbit(w[a / 2 + q + 1], w[a / 2 + q], 16);
+  }
+}
+
+__global__ __launch_bounds__(kFillThreads) void k_fill_level_vec(
+    int64_t lb, const int32_t* __restrict__ w, const int64_t* __restrict__ row_off,
+    const int64_t* __restrict__ pred_ptr, const int32_t* __restrict__ pidx,
+    const int32_t* __restrict__ pdt, const int32_t* __restrict__ pdm,
+    const int32_t* __restrict__ pc, int32_t Beff, const int32_t* __restrict__ ws,
+    uint16_t* __restrict__ m) {
+  using wf::u16x2;
+  const int64_t j = lb + blockIdx.y;
+  const int32_t wj = w[j];
+  const int64_t g = (int64_t)blockIdx.x * kFillThreads + threadIdx.x;
+  // the group's first cell, as t of row j: wj - 8 (g + 1); nothing to do
+  // when the whole group lies before t = 0
+  const int64_t t_first = (int64_t)wj - kVecCells * (g + 1);
+  if (t_first + kVecCells <= 0) return;
+  const int64_t ej = row_off[j] + wj;                 // end of row j (kRowAlign-aligned)
+  const int64_t dst = ej - kVecCells * (g + 1);       // global index of the group's first cell
+  uint32_t acc[4] = {0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
+  const int64_t p0 = pred_ptr[j], p1 = pred_ptr[j + 1];
+  for (int64_t p = p0; p < p1; ++p) {
+    // budget test of Algorithm 1: opt[L, t] + c <= B, i.e. opt[L, t] <= tau
+    const int32_t tau = Beff - pc[p];
+    if (tau < 0) continue;                           // no source cell can pass
+    const int64_t i = pidx[p];
+    const int64_t lo = row_off[i], hi = lo + ws[i];   // readable source cells [lo, hi)
+    const int64_t src = dst + lo - row_off[j] - pdt[p];
+    if (src + kVecCells <= lo || src >= hi) continue;
+    const int32_t a = (int32_t)(src & (kVecCells - 1));
+    const uint4* q = reinterpret_cast<const uint4*>(m + (src - a));
+    const uint4 v0 = q[0], v1 = q[1];
+    const uint32_t wd[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+    uint32_t x[4];
+    switch (a) {
+      case 0: take8<0>(wd, x); break;
+      case 1: take8<1>(wd, x); break;
+      case 2: take8<2>(wd, x); break;
+      case 3: take8<3>(wd, x); break;
+      case 4: take8<4>(wd, x); break;
+      case 5: take8<5>(wd, x); break;
+      case 6: take8<6>(wd, x); break;
+      default: take8<7>(wd, x); break;
+    }
+    if (src < lo || src + kVecCells > hi) {          // the row's edge: cells outside are infinite
+#pragma unroll
+      for (int c = 0; c < kVecCells; c++)
+        if (src + c < lo || src + c >= hi) x[c / 2] |= 0xFFFFu << (16 * (c % 2));
+    }
+    const u16x2 tv = {(unsigned short)tau, (unsigned short)tau};
+    const u16x2 dv = {(unsigned short)pdm[p], (unsigned short)pdm[p]};
+#pragma unroll
+    for (int c = 0; c < 4; c++)
+      acc[c] = __builtin_bit_cast(uint32_t, wf::relax2(__builtin_bit_cast(u16x2, acc[c]),
+                                                       __builtin_bit_cast(u16x2, x[c]), tv, dv));
+  }
+  if (t_first < 0) {                                 // cells before t = 0: padding, infinite
+#pragma unroll
+    for (int c = 0; c < kVecCells; c++)
+      if (t_first + c < 0) acc[c / 2] |= 0xFFFFu << (16 * (c % 2));
+  }
+  *reinterpret_cast<uint4*>(m + dst) = make_uint4(acc[0], acc[1], acc[2], acc[3]);
 }
 
 // The dominance skip of Section 4.2 (last paragraph) on finished rows
@@ -414,11 +502,21 @@ static void fill_levels(rc_solution sol, T* m, hipStream_t s) {
   const int64_t L = (int64_t)f->level_ptr.size() - 1;
   for (int64_t l = 1; l < L; l++) {            // level 0 is the empty set
     const int64_t lb = f->level_ptr[l], le = f->level_ptr[l + 1];
-    const int64_t tiles = (f->level_maxw[l] + kTile - 1) / kTile;
-    if (tiles <= 0 || le <= lb) continue;
-    hipLaunchKernelGGL(k_fill_level<T>, dim3((unsigned)tiles, (unsigned)(le - lb)),
-                       dim3(kFillThreads), 0, s, lb, f->w, f->row_off, f->pred_ptr, f->pidx,
-                       f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, f->w, m);
+    if (le <= lb) continue;
+    if (sizeof(T) == 2) {
+      const int64_t tiles = (f->level_maxw[l] + kVecTile - 1) / kVecTile;
+      if (tiles <= 0) continue;
+      hipLaunchKernelGGL(k_fill_level_vec, dim3((unsigned)tiles, (unsigned)(le - lb)),
+                         dim3(kFillThreads), 0, s, lb, f->w, f->row_off, f->pred_ptr, f->pidx,
+                         f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, f->w,
+                         reinterpret_cast<uint16_t*>(m));
+    } else {
+      const int64_t tiles = (f->level_maxw[l] + kTile - 1) / kTile;
+      if (tiles <= 0) continue;
+      hipLaunchKernelGGL(k_fill_level<T>, dim3((unsigned)tiles, (unsigned)(le - lb)),
+                         dim3(kFillThreads), 0, s, lb, f->w, f->row_off, f->pred_ptr, f->pidx,
+                         f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, f->w, m);
+    }
   }
 }
 

@@ -846,7 +846,21 @@ static int choose_fill_path(rc_family f) {
   // of 2^16 cells and more, and on wide tables of many levels, where one
   // persistent launch beats one launch per level
   if (wide == 2) return 2;
-  if (f->max_row >= 65536) return wide;
+  if (f->max_row >= 65536) {
+    // Between the split-panel wavefront and the level launches on rows of
+    // 2^16 cells and more, by their measured costs on this GPU: the
+    // wavefront runs its 256-cell columns at most three per compute unit at
+    // a time, each through every row of the table at about 2.5 us per row;
+    // a level launch over rows this wide costs about 15 us.  Tables of few
+    // levels and very long rows (the U-Net shape) take the level launches.
+    if (wide != 3) return wide;
+    const int64_t levels = (int64_t)f->level_ptr.size() - 1;
+    const int64_t slots = 3 * (int64_t)num_cus();
+    const int64_t col_rounds = (wide_columns(f) + slots - 1) / slots;
+    const double wave_us = 2.5 * (double)f->F * (double)col_rounds;
+    const double level_us = 15.0 * (double)levels;
+    return level_us < wave_us ? 0 : wide;
+  }
   return (f->max_row >= 8192 && f->level_ptr.size() > 100) ? wide : 0;
 }
 
