@@ -233,26 +233,36 @@ def dual_tables(rcdp, torch, reps=5, names=None):
 
 def dominance_fills(rcdp, torch, reps=5, names=None):
     """rc_solve_dominance (the skip of Section 4.2 on the level fill) against
-    rc_solve on the same family: fill_ms of each (median of reps), and
-    `agrees` = equal (t*, opt[V, t*])."""
+    rc_solve on the same family, with its default fill and with the level
+    fill forced (RCDP_FILL=level: the skip's own cost and gain): fill_ms of
+    each (median of reps), and `agrees` = equal (t*, opt[V, t*])."""
     from paper_1905_11722_amd import workloads
     out = {}
     for name in names or ("resnet50", "unet", "densenet121"):
         case = workloads.case(name)
         g = rcdp.Graph.create(case.graph)
         fam = g.build_family(case.mode)
-        dom, plain = [], []
+        dom, plain, level = [], [], []
+        agrees = True
         for r in range(reps + 1):
             a = fam.solve_dominance(case.B)
             b = fam.solve(case.B, "tc")
+            os.environ["RCDP_FILL"] = "level"
+            try:
+                c = fam.solve(case.B, "tc")
+            finally:
+                os.environ.pop("RCDP_FILL", None)
             if r > 0:
                 dom.append(a.fill_ms())
                 plain.append(b.fill_ms())
-            agrees = (a.t_star, a.m_star) == (b.t_star, b.m_star)
+                level.append(c.fill_ms())
+            agrees = agrees and (a.t_star, a.m_star) == (b.t_star, b.m_star) == (c.t_star, c.m_star)
             a.free()
             b.free()
+            c.free()
         out[name] = {"fill_ms": round(sorted(dom)[len(dom) // 2], 4),
                      "rc_solve_fill_ms": round(sorted(plain)[len(plain) // 2], 4),
+                     "rc_solve_level_fill_ms": round(sorted(level)[len(level) // 2], 4),
                      "agrees": agrees}
         fam.free()
         g.free()

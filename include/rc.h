@@ -58,6 +58,11 @@
  *    (default from the table's width).
  *  - RCDP_DEBUG (any value): the wavefront fills print their launch shape
  *    to stderr.
+ *  - RCDP_JITTER = n (a nonzero integer): the race test.  The persistent
+ *    wavefront fills (k_fill_blocked, k_fill_wide, k_fill_ghost) make their
+ *    waves sleep pseudo-random times drawn from n at block starts and
+ *    before a column publishes its progress, so that columns interleave in
+ *    orders a plain run seldom takes; slower, same results.
  */
 #ifndef RC_H
 #define RC_H

@@ -395,6 +395,7 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p0, const BPa
       }
 
     for (int32_t b = 0; b < p.nblk; ++b) {
+      jitter_delay(p.jitter, c, b, threadIdx.x / kWave);
       const int64_t j0 = 1 + (int64_t)b * kJB;
       const int32_t nrows = meta[(int64_t)b * kMetaInts + 2];
       // the panel of block b + 1: rows before block b, final once the
@@ -565,6 +566,7 @@ __global__ __launch_bounds__(kThreads) void k_fill_blocked(BParams p0, const BPa
       // publish: rows < j0 + nrows of this column are stored
       auto publish = [&]() __attribute__((always_inline)) {
         wait_vm<0>();
+        jitter_delay(p.jitter, c, b, 16);
         if (lane == 0)
           __hip_atomic_store(&progress[c], (int32_t)(j0 + nrows), __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_AGENT);
@@ -675,6 +677,7 @@ hipError_t prepare_table(rc_solution sol, int32_t C, int32_t K, int32_t* ticket,
   prm->ticket = ticket;
   prm->st = sol->status;
   prm->timeout_ticks = wait_ticks();
+  prm->jitter = jitter_seed();
   return hipSuccess;
 }
 

@@ -548,9 +548,9 @@ hipError_t launch_fill_dominance(rc_solution sol, int32_t* we, hipStream_t s) {
   front(0, 1, f->level_maxw[0]);            // the empty set
   for (int64_t l = 1; l < L; l++) {
     const int64_t lb = f->level_ptr[l], le = f->level_ptr[l + 1];
-    const int64_t tiles = (f->level_maxw[l] + kTile - 1) / kTile;
+    const int64_t tiles = (f->level_maxw[l] + kVecTile - 1) / kVecTile;
     if (tiles <= 0 || le <= lb) continue;
-    hipLaunchKernelGGL(k_fill_level<uint16_t>, dim3((unsigned)tiles, (unsigned)(le - lb)),
+    hipLaunchKernelGGL(k_fill_level_vec, dim3((unsigned)tiles, (unsigned)(le - lb)),
                        dim3(kFillThreads), 0, s, lb, f->w, f->row_off, f->pred_ptr, f->pidx,
                        f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, (const int32_t*)we, sol->m);
     front(lb, le - lb, f->level_maxw[l]);

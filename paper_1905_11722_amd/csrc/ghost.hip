@@ -153,6 +153,7 @@ __global__ __launch_bounds__(kGT) void k_fill_ghost(GParams p0, const GParams* g
     };
 
     for (int32_t b = 0; b < p.nblk; ++b) {
+      jitter_delay(p.jitter, c, b, tid / kWave);
       cint32* const mt = meta + (int64_t)b * kMetaInts;
       const int32_t s0 = bstart[b], s1 = bstart[b + 1];
       if (cC > mt[3]) {                              // no row of the block reaches the column
@@ -323,6 +324,7 @@ __global__ __launch_bounds__(kGT) void k_fill_ghost(GParams p0, const GParams* g
         // ---------------- publish: rows < s1 of this column are stored
         wait_vm<0>();
         bar();
+        jitter_delay(p.jitter, c, b, 16);
         if (tid == 0)
           __hip_atomic_store(&progress[c], s1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         return true;
@@ -479,6 +481,7 @@ hipError_t prepare_table(rc_solution sol, int32_t C, int32_t K, int32_t* ticket,
   prm->ticket = ticket;
   prm->st = sol->status;
   prm->timeout_ticks = wait_ticks();
+  prm->jitter = jitter_seed();
   return hipSuccess;
 }
 

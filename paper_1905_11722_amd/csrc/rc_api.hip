@@ -40,6 +40,11 @@ void set_last_error_msg(const char* msg) {
   std::snprintf(g_last_error, sizeof(g_last_error), "%s", msg);
 }
 
+int32_t jitter_seed() {
+  const char* env = std::getenv("RCDP_JITTER");
+  return env ? (int32_t)std::strtol(env, nullptr, 10) : 0;
+}
+
 namespace {
 // Free pinned buffers, smallest first: a request takes the smallest that
 // fits, or allocates a power of two of at least 64 KB.  Never destroyed, so

@@ -223,6 +223,10 @@ namespace rcdp {
 void set_last_error(const char* what, hipError_t e);
 void set_last_error_msg(const char* msg);
 
+// Seed of the wavefront fills' random delays (the race test), from the
+// environment switch RCDP_JITTER; 0 (unset): no delays (rc_api.hip).
+int32_t jitter_seed();
+
 // Pinned host memory for the copies between host and device inside one
 // call (rc_api.hip).  A copy to or from pinned memory is asynchronous, so
 // the copies of a call cost one synchronisation of the stream; a copy to or
@@ -318,6 +322,7 @@ struct BParams {
   const int32_t* push;                   // [nblk * kJB * kPushInts]
   const int32_t* live;                   // [nblk * cap * 2] live panel records per column
   int32_t cap;
+  int32_t jitter;                        // race test: seed of random delays (0: none)
   const uint16_t* sentinel;              // 8 cells of infinity
   uint16_t* m;
   int32_t* progress;
@@ -341,6 +346,7 @@ struct GParams {
   const int32_t* tri;                    // [nblk * kJB * kTriInts]
   const int32_t* live;                   // [nblk * cap * 2] live panel records per column
   int32_t cap;
+  int32_t jitter;                        // race test: seed of random delays (0: none)
   const uint16_t* sentinel;              // 8 cells of infinity
   uint16_t* m;
   int32_t* progress;
@@ -407,7 +413,7 @@ struct WParams {
   uint16_t* m;
   int64_t m_bytes;                       // the table with its trailing guard
   int32_t null_off;                      // byte offset of the trailing guard
-  int32_t pad0;
+  int32_t jitter;                        // race test: seed of random delays (0: none)
   int32_t* progress;
   int32_t* ticket;
   DevStatus* st;

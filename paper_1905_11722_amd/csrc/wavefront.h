@@ -117,6 +117,23 @@ __device__ __forceinline__ u16x2 relax2(u16x2 acc, u16x2 x, u16x2 tau, u16x2 dm)
   return __builtin_elementwise_min(acc, r);
 }
 
+// The race test's delay (seed != 0): at one in four of the points a wave
+// passes, it sleeps a pseudo-random 0..63 rounds, drawn from the seed, the
+// column, the block and the point, so that the order in which columns and
+// waves store, publish and poll changes from one seed to the next while the
+// table must not.
+__device__ __forceinline__ void jitter_delay(int32_t seed, int32_t c, int32_t b, int32_t point) {
+  if (seed == 0) return;
+  uint32_t h = (uint32_t)seed * 0x9E3779B1u ^ (uint32_t)c * 0x85EBCA77u ^
+               (uint32_t)(b + 2) * 0xC2B2AE3Du ^ (uint32_t)point * 0x27D4EB2Fu;
+  h ^= h >> 15;
+  h *= 0x2C1B3C6Du;
+  h ^= h >> 12;
+  h = __builtin_amdgcn_readfirstlane(h);
+  if ((h & 3) != 0) return;
+  for (uint32_t r = (h >> 2) & 63; r > 0; r--) __builtin_amdgcn_s_sleep(4);
+}
+
 // The parameters of table tk % nb of a batched launch, read through the
 // constant address space so that they load into scalar registers like the
 // kernel arguments of a single-table launch (nb == 1: p0 itself).

@@ -395,6 +395,7 @@ __attribute__((amdgpu_waves_per_eu((3 * (NP + 1) + 3) / 4))) void k_fill_wide(WP
     for (int32_t b = -1; b < p.nblk; b++) {
       const int32_t pb = b + 1;
       bool ok = true;
+      jitter_delay(p.jitter, c, b, wave);
       if (wave == 0) {
         if (b >= 0) {
           const int32_t nrows = meta[b * kWMeta + 2];
@@ -440,6 +441,7 @@ __attribute__((amdgpu_waves_per_eu((3 * (NP + 1) + 3) / 4))) void k_fill_wide(WP
             s_rows.acc[q][lane + 64 * k] = __builtin_bit_cast(uint32_t, m);
             s_rows.nxt[q][lane + 64 * k] = kInfPair;
           }
+        jitter_delay(p.jitter, c, b, NP + 1);
         if (b >= 0 && lane == 0)
           __hip_atomic_store(&p.progress[c], 1 + (b + 1) * kJB < p.F ? 1 + (b + 1) * kJB : p.F,
                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -767,6 +769,7 @@ static hipError_t prepare_wide(rc_solution sol, int32_t K, int32_t* ticket, WPar
   prm->ticket = ticket;
   prm->st = sol->status;
   prm->timeout_ticks = wait_ticks();
+  prm->jitter = jitter_seed();
   return hipSuccess;
 }
 

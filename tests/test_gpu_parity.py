@@ -342,6 +342,30 @@ def test_wavefront_repeated_solves(rc, oracle_mod, monkeypatch, path, seed):
                 sol.free()
 
 
+@pytest.mark.parametrize("path", ["wavefront", "wide", "ghost"])
+@pytest.mark.parametrize("jitter", [1, 2, 3, 7])
+def test_wavefront_race_delays(rc, oracle_mod, monkeypatch, path, jitter):
+    """The race test: with RCDP_JITTER set, every wave of a persistent fill
+    sleeps a pseudo-random time (drawn from the seed, its column, block and
+    point) at one in four of its block starts and before a column publishes
+    its progress, so that columns store, publish and poll in orders a plain
+    run seldom takes.  Every table, t* and schedule must still be the
+    oracle's, for both families at three budgets, and in a batch."""
+    monkeypatch.setenv("RCDP_FILL", path)
+    monkeypatch.setenv("RCDP_JITTER", str(jitter))
+    g = W.random_dag(12, 0.45, 5100 + jitter, tmax=700, mmax=60)
+    lo, hi = 2 * max(g.M), 2 * sum(g.M)
+    for B in (lo, (2 * lo + hi) // 3, hi):
+        for mode in ("exact", "pruned"):
+            compare(rc, oracle_mod, g, mode, B)
+    fam = rc.Graph.create(g).build_family("pruned")
+    for B, sol in fam.sweep([lo, (lo + hi) // 2, hi], "tc"):
+        rm, _ = oracle_mod.solve(g, "pruned", B, "tc").table()
+        m, _ = sol.table()
+        np.testing.assert_array_equal(m, rm, err_msg=f"batch B={B}")
+        sol.free()
+
+
 @pytest.mark.parametrize("path", PATHS)
 def test_fill_paths_long_chain(rc, oracle_mod, monkeypatch, path):
     """A long chain: one target per level, rows of many columns."""
