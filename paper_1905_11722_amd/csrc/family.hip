@@ -7,6 +7,8 @@
 // are lane-local popcount-style loops followed by a wave reduction.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "rc_internal.h"
 
 namespace rcdp {
@@ -36,6 +38,20 @@ __device__ __forceinline__ int64_t word_cost(uint64_t bits, int word, const int3
 }
 
 // ---------------------------------------------------------------- graph
+
+// Gathers up to kPackMax device segments (whole 32-bit words) into one
+// buffer, so that the results a host call reads back cost one copy; block
+// row y copies segment y.
+__global__ __launch_bounds__(256) void k_pack(PackList L, uint32_t* dst) {
+  if ((int)blockIdx.y >= L.n) return;
+  const PackSeg sg = L.seg[blockIdx.y];
+  const uint32_t* src = static_cast<const uint32_t*>(sg.src);
+  uint32_t* out = dst + sg.dst_off / 4;
+  const int64_t words = sg.bytes / 4;
+  for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < words;
+       x += (int64_t)gridDim.x * blockDim.x)
+    out[x] = src[x];
+}
 
 __global__ void k_zero_u64(uint64_t* p, int64_t count) {
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count;
@@ -705,6 +721,16 @@ __global__ __launch_bounds__(1024) void k_sum(const int64_t* in, int64_t count, 
 }  // namespace
 
 // ============================================================== launchers
+
+hipError_t launch_pack(const PackList& L, void* dst, hipStream_t s) {
+  if (L.n <= 0) return hipSuccess;
+  int64_t most = 0;
+  for (int q = 0; q < L.n; q++) most = std::max<int64_t>(most, L.seg[q].bytes / 4);
+  const unsigned gx = (unsigned)std::max<int64_t>(1, std::min<int64_t>((most + 255) / 256, 64));
+  hipLaunchKernelGGL(k_pack, dim3(gx, (unsigned)L.n), dim3(256), 0, s, L,
+                     static_cast<uint32_t*>(dst));
+  return hipGetLastError();
+}
 
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s) {
   hipLaunchKernelGGL(k_zero_u64, dim3(1), dim3(256), 0, s, static_cast<uint64_t*>(p),

@@ -430,6 +430,16 @@ static int64_t pruned_family_size(rc_graph g) {
   return (int64_t)g->n + 1 + (g->num_sinks > 1 ? 1 : 0);
 }
 
+// Gathers L into the device buffer dev (at least bytes) and enqueues one
+// copy of it into the staging buffer.
+static int pack_to_host(const PackList& L, void* dev, size_t bytes, Staging& st, hipStream_t s) {
+  if (launch_pack(L, dev, s) != hipSuccess) return RC_E_DEVICE;
+  st.in_flight();
+  if (hipMemcpyAsync(st.data(), dev, bytes, hipMemcpyDeviceToHost, s) != hipSuccess)
+    return RC_E_DEVICE;
+  return RC_OK;
+}
+
 // Record buffers up to this many records are sized from an upper bound
 // (every record holds at least one pair) without waiting for their count.
 constexpr int64_t kRecordBound = (int64_t)1 << 18;
@@ -533,17 +543,16 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
                o_pp = L1.add<int64_t>(F + 1);
   {
     Staging st1(L1.bytes);
-    if (!st1.data()) return RC_E_NOMEM;
-    st1.in_flight();
-    RC_HIP(hipMemcpyAsync(st1.at<char>(o_st), f->status, sizeof(DevStatus),
-                          hipMemcpyDeviceToHost, s));
-    RC_HIP(hipMemcpyAsync(st1.at<char>(o_size), f->size, sizeof(int32_t) * F,
-                          hipMemcpyDeviceToHost, s));
-    RC_HIP(hipMemcpyAsync(st1.at<char>(o_w), f->w, sizeof(int32_t) * F, hipMemcpyDeviceToHost, s));
-    RC_HIP(hipMemcpyAsync(st1.at<char>(o_off), f->row_off, sizeof(int64_t) * (F + 1),
-                          hipMemcpyDeviceToHost, s));
-    RC_HIP(hipMemcpyAsync(st1.at<char>(o_pp), f->pred_ptr, sizeof(int64_t) * (F + 1),
-                          hipMemcpyDeviceToHost, s));
+    void* pk1 = tmp.get(L1.bytes);
+    if (!st1.data() || !pk1) return RC_E_NOMEM;
+    PackList P1;
+    P1.add(f->status, sizeof(DevStatus), (int64_t)o_st);
+    P1.add(f->size, sizeof(int32_t) * F, (int64_t)o_size);
+    P1.add(f->w, sizeof(int32_t) * F, (int64_t)o_w);
+    P1.add(f->row_off, sizeof(int64_t) * (F + 1), (int64_t)o_off);
+    P1.add(f->pred_ptr, sizeof(int64_t) * (F + 1), (int64_t)o_pp);
+    const int pc1 = pack_to_host(P1, pk1, L1.bytes, st1, s);
+    if (pc1 != RC_OK) return pc1;
     const int ss = sync_landed(st1);
     if (ss != RC_OK) return ss;
     const DevStatus& h1 = *st1.at<DevStatus>(o_st);
@@ -672,22 +681,18 @@ static int build_family_impl(rc_family f, int64_t max_sets, hipStream_t s) {
                q_clu = L4.add<int64_t>(1), q_wrec = L4.add<int64_t>(1),
                q_wc = L4.add<int64_t>(wcounts ? f->nblk : 0);
   Staging st4(L4.bytes);
-  if (!st4.data()) return RC_E_NOMEM;
-  st4.in_flight();
-  RC_HIP(hipMemcpyAsync(st4.at<char>(q_st), f->status, sizeof(DevStatus), hipMemcpyDeviceToHost,
-                        s));
-  if (f->nblk > 0)
-    RC_HIP(hipMemcpyAsync(st4.at<char>(q_rec), f->rec_ptr + f->nblk, sizeof(int64_t),
-                          hipMemcpyDeviceToHost, s));
-  if (records)
-    RC_HIP(hipMemcpyAsync(st4.at<char>(q_clu), f->clu_ptr + f->nblk, sizeof(int64_t),
-                          hipMemcpyDeviceToHost, s));
+  void* pk4 = tmp.get(L4.bytes);
+  if (!st4.data() || !pk4) return RC_E_NOMEM;
+  PackList P4;
+  P4.add(f->status, sizeof(DevStatus), (int64_t)q_st);
+  if (f->nblk > 0) P4.add(f->rec_ptr + f->nblk, sizeof(int64_t), (int64_t)q_rec);
+  if (records) P4.add(f->clu_ptr + f->nblk, sizeof(int64_t), (int64_t)q_clu);
   if (wcounts) {
-    RC_HIP(hipMemcpyAsync(st4.at<char>(q_wrec), f->wrec_ptr + f->nblk, sizeof(int64_t),
-                          hipMemcpyDeviceToHost, s));
-    RC_HIP(hipMemcpyAsync(st4.at<char>(q_wc), wcounts, sizeof(int64_t) * (size_t)f->nblk,
-                          hipMemcpyDeviceToHost, s));
+    P4.add(f->wrec_ptr + f->nblk, sizeof(int64_t), (int64_t)q_wrec);
+    P4.add(wcounts, sizeof(int64_t) * f->nblk, (int64_t)q_wc);
   }
+  const int pc4 = pack_to_host(P4, pk4, L4.bytes, st4, s);
+  if (pc4 != RC_OK) return pc4;
   const int ss = sync_landed(st4);
   if (ss != RC_OK) return ss;
   if (up_stage) up_stage->landed();
@@ -1180,19 +1185,16 @@ int rc_reconstruct(rc_solution sol, void* stream, int32_t* k, int32_t* chain_hos
   const size_t o_st = lay.add<DevStatus>(1), o_ch = lay.add<int32_t>(kmax),
                o_sg = lay.add<int32_t>(n), o_ca = lay.add<uint8_t>(n);
   Staging stage(lay.bytes);
-  if (!stage.data()) return RC_E_NOMEM;
+  if (!sol->pack) sol->pack = sol->arena.get(lay.bytes);
+  if (!stage.data() || !sol->pack) return RC_E_NOMEM;
   RC_HIP(launch_trace(sol, s));
-  stage.in_flight();
-  RC_HIP(hipMemcpyAsync(stage.at<char>(o_st), sol->status, sizeof(DevStatus),
-                        hipMemcpyDeviceToHost, s));
-  if (kmax > 0)
-    RC_HIP(hipMemcpyAsync(stage.at<char>(o_ch), sol->chain, sizeof(int32_t) * (size_t)kmax,
-                          hipMemcpyDeviceToHost, s));
-  if (n > 0) {
-    RC_HIP(hipMemcpyAsync(stage.at<char>(o_sg), sol->seg, sizeof(int32_t) * n,
-                          hipMemcpyDeviceToHost, s));
-    RC_HIP(hipMemcpyAsync(stage.at<char>(o_ca), sol->cached, n, hipMemcpyDeviceToHost, s));
-  }
+  PackList PL;
+  PL.add(sol->status, sizeof(DevStatus), (int64_t)o_st);
+  PL.add(sol->chain, sizeof(int32_t) * kmax, (int64_t)o_ch);
+  PL.add(sol->seg, sizeof(int32_t) * n, (int64_t)o_sg);
+  PL.add(sol->cached, (n + 3) / 4 * 4, (int64_t)o_ca);   // whole words of the padded buffer
+  const int pc = pack_to_host(PL, sol->pack, lay.bytes, stage, s);
+  if (pc != RC_OK) return pc;
   RC_HIP(hipStreamSynchronize(s));
   stage.landed();
   const DevStatus hs = *stage.at<DevStatus>(o_st);

@@ -190,6 +190,7 @@ struct rc_solution_s {
   int32_t* chain = nullptr;       // [F]
   int32_t* seg = nullptr;         // [n]
   uint8_t* cached = nullptr;      // [n]
+  void* pack = nullptr;           // the traceback's results gathered for one copy to the host
   int32_t* progress = nullptr;    // blocked fill: rows finished per column
   int32_t* ticket = nullptr;      // blocked fill: next column to take
   int32_t* crec = nullptr;        // blocked fill: compact live records [clu_total * kRecInts]
@@ -267,6 +268,22 @@ struct StageLayout {
 
 // ---- utilities (family.hip)
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);  // bytes % 8 == 0
+// Device segments gathered into one device buffer (whole 32-bit words; the
+// byte counts, offsets and pointers are multiples of 4).
+struct PackSeg {
+  const void* src;
+  int64_t bytes;
+  int64_t dst_off;
+};
+constexpr int kPackMax = 8;
+struct PackList {
+  PackSeg seg[kPackMax];
+  int32_t n = 0;
+  void add(const void* src, int64_t bytes, int64_t dst_off) {
+    if (bytes > 0) seg[n++] = PackSeg{src, bytes, dst_off};
+  }
+};
+hipError_t launch_pack(const PackList& L, void* dst, hipStream_t s);
 
 // ---- graph kernels (family.hip)
 hipError_t launch_graph_masks(rc_graph g, const int32_t* d_row_ptr, const int32_t* d_col_idx,
