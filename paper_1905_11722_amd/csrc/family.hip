@@ -339,31 +339,63 @@ __global__ __launch_bounds__(256) void k_rank(int words, int n, const uint64_t* 
 
 // Pruned family: candidates are [0] the empty set, [1..n] the sets L^v
 // (pairwise distinct), [n+1] V, which is dropped when some L^v already
-// equals V.  One workgroup: candidate sizes in LDS, then every candidate
-// counts the candidates before it (smaller size, or equal size and smaller
-// numeric value).
+// equals V.  One workgroup: the candidates are bucketed by size (a counting
+// sort in LDS), and a candidate's index is the number of candidates of
+// smaller size plus those of its own size with a smaller numeric value.
 __global__ __launch_bounds__(1024) void k_rank_pruned(int words, int n, const uint64_t* cand,
                                                       uint64_t* bits, int64_t fstride,
                                                       DevStatus* st) {
+  constexpr int kThreads = 1024;
   __shared__ int32_t s_sz[kMaxNodes + 2];
+  __shared__ int32_t s_start[kMaxNodes + 2];   // candidates of size < s, s = 0..n+1
+  __shared__ int32_t s_next[kMaxNodes + 2];    // next free slot of each size's bucket
+  __shared__ int32_t s_list[kMaxNodes + 2];    // candidates grouped by size
+  __shared__ int32_t s_wsum[kThreads / kWave];
   __shared__ int32_t s_vdup;
-  const int64_t total = (int64_t)n + 2;
-  if (threadIdx.x == 0) s_vdup = n == 0;             // V is the empty set itself
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1), wave = tid / kWave;
+  const int total = n + 2, bins = n + 2;       // sizes 0..n, counted one bin up
+  if (tid == 0) s_vdup = n == 0;                 // V is the empty set itself
+  for (int x = tid; x < bins; x += kThreads) s_start[x] = 0;
+  for (int x = tid; x < total; x += kThreads) s_sz[x] = popcnt_set(cand + (int64_t)x * words, words);
   __syncthreads();
-  for (int64_t x = threadIdx.x; x < total; x += blockDim.x)
-    s_sz[x] = popcnt_set(cand + x * words, words);
+  for (int x = 1 + tid; x <= n; x += kThreads)
+    if (s_sz[x] == n) s_vdup = 1;                 // some L^v is V already
   __syncthreads();
-  for (int64_t x = 1 + threadIdx.x; x <= n; x += blockDim.x)
-    if (s_sz[x] == n) s_vdup = 1;                     // some L^v is V already
+  const int valid = s_vdup ? n + 1 : n + 2;
+  for (int x = tid; x < valid; x += kThreads) atomicAdd(&s_start[s_sz[x] + 1], 1);
   __syncthreads();
-  const int64_t valid = s_vdup ? n + 1 : n + 2;
-  for (int64_t x = threadIdx.x; x < valid; x += blockDim.x) {
-    const uint64_t* X = cand + x * words;
+  // inclusive scan of the counts: s_start[s] = candidates of size < s
+  const int per = (bins + kThreads - 1) / kThreads;
+  const int b0 = min(bins, tid * per), b1 = min(bins, b0 + per);
+  int run = 0;
+  for (int q = b0; q < b1; q++) {
+    run += s_start[q];
+    s_start[q] = run;
+  }
+  int incl = run;
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int y = __shfl_up(incl, off, kWave);
+    if (lane >= off) incl += y;
+  }
+  if (lane == kWave - 1) s_wsum[wave] = incl;
+  __syncthreads();
+  int before = incl - run;
+  for (int q = 0; q < wave; q++) before += s_wsum[q];
+  for (int q = b0; q < b1; q++) {
+    s_start[q] += before;
+    s_next[q] = s_start[q];
+  }
+  __syncthreads();
+  for (int x = tid; x < valid; x += kThreads) s_list[atomicAdd(&s_next[s_sz[x]], 1)] = x;
+  __syncthreads();
+  for (int x = tid; x < valid; x += kThreads) {
+    const uint64_t* X = cand + (int64_t)x * words;
     const int sx = s_sz[x];
-    int64_t rank = 0;
-    for (int64_t y = 0; y < valid; y++) {
-      const int sy = s_sz[y];
-      if (y != x && (sy < sx || (sy == sx && cmp_value(cand + y * words, X, words) < 0))) rank++;
+    int64_t rank = s_start[sx];
+    for (int q = s_start[sx]; q < s_start[sx + 1]; q++) {
+      const int y = s_list[q];
+      if (y != x && cmp_value(cand + (int64_t)y * words, X, words) < 0) rank++;
     }
     if (rank >= fstride) {
       st->error = 1;
@@ -371,7 +403,7 @@ __global__ __launch_bounds__(1024) void k_rank_pruned(int words, int n, const ui
     }
     for (int w = 0; w < words; w++) bits[(int64_t)w * fstride + rank] = X[w];
   }
-  if (threadIdx.x == 0) st->count = valid;
+  if (tid == 0) st->count = valid;
 }
 
 // ------------------------------------------------------- per-set values
