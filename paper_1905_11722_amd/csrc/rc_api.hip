@@ -365,9 +365,9 @@ void rc_graph_free(rc_graph g) {
 // Which blocks the family's wavefront records use.  RCDP_FILL=wavefront
 // forces the row-push fill's fixed blocks and RCDP_FILL=ghost the ghost-zone
 // blocks (families of at most kGhostMaxSets sets).  Otherwise: fixed blocks
-// for families beyond that size and for tables with rows of 2^16 cells and
-// more (where the split-panel fill measured fastest), ghost-zone blocks for
-// the rest.
+// for families beyond that size, for families of kWideMinSets sets and more
+// and for tables with rows of 2^16 cells and more (where the split-panel
+// fill measured fastest), ghost-zone blocks for the rest.
 // shape_known: max_row and the levels are set (after the host copies).
 static int32_t family_block_kind(rc_family f, bool shape_known) {
   const int64_t F = f->F;
@@ -378,9 +378,12 @@ static int32_t family_block_kind(rc_family f, bool shape_known) {
     return kBlocksFixed;
   if (env && std::strcmp(env, "ghost") == 0) return kBlocksGhost;
   if (!shape_known) return -1;                 // decided once the table's shape is known
-  // rows of 2^16 cells and more: fixed blocks, so that the split-panel fill
-  // (measured fastest on every such table here) can take the family
-  return f->max_row >= 65536 ? kBlocksFixed : kBlocksGhost;
+  // fixed blocks, so that the split-panel fill can take the family, for
+  // rows of 2^16 cells and more and for families of kWideMinSets sets and
+  // more (measured faster than the ghost-zone fill on every such shape
+  // here: the ghost blocks hold fewer rows, so that each staged window
+  // serves fewer targets); ghost-zone blocks for the smaller families
+  return f->max_row >= 65536 || F >= kWideMinSets ? kBlocksFixed : kBlocksGhost;
 }
 
 // Block starts of the chosen kind (host).
@@ -871,6 +874,7 @@ static int choose_fill_path(rc_family f) {
     const double level_us = 15.0 * (double)levels;
     return level_us < wave_us ? 0 : wide;
   }
+  if (wide == 3 && f->F <= kGhostMaxSets) return 3;
   return (f->max_row >= 8192 && f->level_ptr.size() > 100) ? wide : 0;
 }
 
