@@ -44,6 +44,7 @@ FILL_SOURCES = {
                     _CSRC + "rc_internal.h"],
     "k_fill_ghost": [_CSRC + "ghost.hip", _CSRC + "blocks.hip", _CSRC + "wavefront.h",
                      _CSRC + "rc_internal.h", _CSRC + "ghost_cut.h"],
+    "k_fill_level_vec": [_CSRC + "fill.hip", _CSRC + "wavefront.h", _CSRC + "rc_internal.h"],
     "k_fill_level": [_CSRC + "fill.hip", _CSRC + "rc_internal.h"],
 }
 

@@ -236,7 +236,7 @@ void rc_family_free(rc_family f);
  *  *t_opt, *m_opt: t* and opt[V, t*], or -1 and -1 when infeasible.
  * Cells are 16 bits wide while min(B, 2 M(V)) <= 65532 (every fill path);
  * above that the table takes 32-bit cells and the one-launch-per-level fill
- * (rc_solution_fill_path reports 0), with the same results.
+ * (rc_solution_fill_path reports 4), with the same results.
  * Returns RC_OK or RC_INFEASIBLE (both create *out, whose table can be
  * exported), or an error: RC_E_ARG, RC_E_OVERFLOW (min(B, 2 M(V)) > 2^30,
  * which rc_graph_create's limit on M(V) rules out), RC_E_NOMEM, RC_E_DEVICE.
@@ -288,10 +288,11 @@ int rc_solution_fill_ms(rc_solution s, float* ms);
  * rc_solution_fill_ms.  Returns RC_OK or RC_E_ARG (NULL argument). */
 int rc_solution_fill_kernel_ms(rc_solution s, float* ms);
 /* Which fill the solve ran (all of them compute the same table, Algorithm 1
- * of Section 4.2): *path = 0 one launch per group of equal-size sets
- * (k_fill_level_vec / k_fill_level), 1 the persistent row-push wavefront
+ * of Section 4.2): *path = 0 one launch per group of equal-size sets on
+ * 16-bit cells (k_fill_level_vec), 1 the persistent row-push wavefront
  * (k_fill_blocked), 2 the ghost-zone wavefront (k_fill_ghost), 3 the
- * split-panel wavefront (k_fill_wide).  Returns RC_OK or RC_E_ARG (NULL
+ * split-panel wavefront (k_fill_wide), 4 one launch per group of equal-size
+ * sets on 32-bit cells (k_fill_level).  Returns RC_OK or RC_E_ARG (NULL
  * argument). */
 int rc_solution_fill_path(rc_solution s, int32_t* path);
 

@@ -1171,7 +1171,7 @@ int rc_solution_fill_kernel_ms(rc_solution s, float* ms) {
 
 int rc_solution_fill_path(rc_solution s, int32_t* path) {
   if (!s || !path) return RC_E_ARG;
-  *path = s->fill_path;
+  *path = s->fill_path == 0 && s->cell32 ? 4 : s->fill_path;
   return RC_OK;
 }
 

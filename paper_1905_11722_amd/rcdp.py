@@ -389,7 +389,8 @@ class Solution:
                "rc_solution_fill_kernel_ms")
         return ms.value
 
-    FILL_KERNELS = ("k_fill_level", "k_fill_blocked", "k_fill_ghost", "k_fill_wide")
+    FILL_KERNELS = ("k_fill_level_vec", "k_fill_blocked", "k_fill_ghost", "k_fill_wide",
+                    "k_fill_level")
 
     def fill_kernel(self):
         """Name of the fill kernel the solve ran (see rc_solution_fill_path)."""

@@ -270,7 +270,7 @@ def test_fill_paths_small_cases(rc, oracle_mod, monkeypatch, path, name):
         compare(rc, oracle_mod, g, c.mode, B)
 
 
-@pytest.mark.parametrize("path,kernel", [("level", "k_fill_level"),
+@pytest.mark.parametrize("path,kernel", [("level", "k_fill_level_vec"),
                                          ("wavefront", "k_fill_blocked"),
                                          ("wide", "k_fill_wide"), ("ghost", "k_fill_ghost")])
 def test_fill_path_is_reported(rc, monkeypatch, path, kernel):
