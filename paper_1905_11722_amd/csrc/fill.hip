@@ -118,18 +118,29 @@ __global__ __launch_bounds__(kFillThreads) void k_fill_level(
   }
 }
 
-// The level fill for 16-bit cells, eight cells per thread, two per packed
+// The level fill for 16-bit cells, eight cells per lane, two per packed
 // instruction.  Cells are counted from the row's end, which lies on a
-// kRowAlign boundary: thread group g of target j owns the cells at
+// kRowAlign boundary: lane group g of target j owns the cells at
 // [E_j - 8 (g + 1), E_j - 8 g) (E_j = end of the row), one aligned 16-byte
 // store, and the source cell of target cell x along a pair is x + D with
 // D = row_off[i] - row_off[j] - dt, the same for every cell of the pair.
 // So a pair's eight source cells start D mod 8 cells past an aligned
 // 16-byte word: two aligned loads and a shift by that uniform amount.
 // Source cells outside [0, ws[i]) and target cells before the row's first
-// cell read as infinity.  ws as for k_fill_level.
+// cell read as infinity.
+//
+// The NW waves of a workgroup own the same 512 cells and take every NW-th
+// group of kLevelGroup pairs; their minima meet in LDS.  A group's
+// records arrive in one vector load (word k on lane k) and are broadcast to
+// scalar registers, then every source load of the group goes out before the
+// first is used (a pair a lane skips loads the lane's own cells instead),
+// so that a lane waits for memory twice per group, and the chain of groups
+// a wave walks is 1/NW of the target's pairs.  With kFront the
+// readable part of a source row is ws[i] (the dominance skip's front).
 constexpr int kVecCells = 8;
-constexpr int kVecTile = kFillThreads * kVecCells;
+constexpr int kVecTile = kWave * kVecCells;          // cells per workgroup
+constexpr int kLevelGroup = 4;
+static_assert(sizeof(LevelPair) == 32 && kLevelGroup * 8 <= 32, "a group's records on 32 lanes");
 
 // words w[0..7] hold cells 0..15 of two aligned 16-byte loads; out[q] gets
 // cells a + 2q and a + 2q + 1 (a uniform, 0..7)
@@ -144,58 +155,107 @@ __device__ __forceinline__ void take8(const uint32_t (&w)[8], uint32_t (&out)[4]
   }
 }
 
-__global__ __launch_bounds__(kFillThreads) void k_fill_level_vec(
+template <bool kFront, int NW>
+__global__ __launch_bounds__(NW * kWave) void k_fill_level_vec(
     int64_t lb, const int32_t* __restrict__ w, const int64_t* __restrict__ row_off,
-    const int64_t* __restrict__ pred_ptr, const int32_t* __restrict__ pidx,
-    const int32_t* __restrict__ pdt, const int32_t* __restrict__ pdm,
-    const int32_t* __restrict__ pc, int32_t Beff, const int32_t* __restrict__ ws,
-    uint16_t* __restrict__ m) {
+    const int64_t* __restrict__ pred_ptr, const LevelPair* __restrict__ lp, int32_t Beff,
+    const int32_t* __restrict__ ws, uint16_t* __restrict__ m) {
   using wf::u16x2;
+  constexpr int kLevelWaves = NW;
+  __shared__ uint4 s_acc[kLevelWaves > 1 ? kLevelWaves - 1 : 1][kWave];
   const int64_t j = lb + blockIdx.y;
   const int32_t wj = w[j];
-  const int64_t g = (int64_t)blockIdx.x * kFillThreads + threadIdx.x;
-  // the group's first cell, as t of row j: wj - 8 (g + 1); nothing to do
-  // when the whole group lies before t = 0
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  const int64_t g = (int64_t)blockIdx.x * kWave + lane;
+  // the group's first cell, as t of row j: wj - 8 (g + 1); nothing to store
+  // when the whole group lies before t = 0.  Such a lane still runs the loop
+  // (on the row's last group), since the records reach every lane of the wave
+  // from lanes 0..31; a workgroup with no such lane leaves at once.
   const int64_t t_first = (int64_t)wj - kVecCells * (g + 1);
-  if (t_first + kVecCells <= 0) return;
-  const int64_t ej = row_off[j] + wj;                 // end of row j (kRowAlign-aligned)
-  const int64_t dst = ej - kVecCells * (g + 1);       // global index of the group's first cell
+  const bool live = t_first + kVecCells > 0;
+  if ((int64_t)wj - kVecCells * ((int64_t)blockIdx.x * kWave) <= 0) return;  // lane 0's group
+  const int64_t rj = row_off[j];
+  // the group's first cell (aligned: the row ends on a kRowAlign boundary)
+  const int64_t dst = rj + wj - kVecCells * (live ? g + 1 : 1);
   uint32_t acc[4] = {0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
   const int64_t p0 = pred_ptr[j], p1 = pred_ptr[j + 1];
-  for (int64_t p = p0; p < p1; ++p) {
-    // budget test of Algorithm 1: opt[L, t] + c <= B, i.e. opt[L, t] <= tau
-    const int32_t tau = Beff - pc[p];
-    if (tau < 0) continue;                           // no source cell can pass
-    const int64_t i = pidx[p];
-    const int64_t lo = row_off[i], hi = lo + ws[i];   // readable source cells [lo, hi)
-    const int64_t src = dst + lo - row_off[j] - pdt[p];
-    if (src + kVecCells <= lo || src >= hi) continue;
-    const int32_t a = (int32_t)(src & (kVecCells - 1));
-    const uint4* q = reinterpret_cast<const uint4*>(m + (src - a));
-    const uint4 v0 = q[0], v1 = q[1];
-    const uint32_t wd[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-    uint32_t x[4];
-    switch (a) {
-      case 0: take8<0>(wd, x); break;
-      case 1: take8<1>(wd, x); break;
-      case 2: take8<2>(wd, x); break;
-      case 3: take8<3>(wd, x); break;
-      case 4: take8<4>(wd, x); break;
-      case 5: take8<5>(wd, x); break;
-      case 6: take8<6>(wd, x); break;
-      default: take8<7>(wd, x); break;
-    }
-    if (src < lo || src + kVecCells > hi) {          // the row's edge: cells outside are infinite
+  for (int64_t pg = p0 + (int64_t)wave * kLevelGroup; pg < p1;
+       pg += (int64_t)kLevelWaves * kLevelGroup) {
+    // the group's records (the array has kLevelGroup more at its end) in one
+    // vector load, word k on lane k, then broadcast to scalar registers
+    const int32_t word = reinterpret_cast<const int32_t*>(lp + pg)[lane & 31];
+    LevelPair r[kLevelGroup];
 #pragma unroll
-      for (int c = 0; c < kVecCells; c++)
-        if (src + c < lo || src + c >= hi) x[c / 2] |= 0xFFFFu << (16 * (c % 2));
+    for (int q = 0; q < kLevelGroup; q++) {
+      auto rd = [&](int k) { return __builtin_amdgcn_readlane(word, 8 * q + k); };
+      r[q].lo = (int64_t)(((uint64_t)(uint32_t)rd(1) << 32) | (uint32_t)rd(0));
+      r[q].base = (int64_t)(((uint64_t)(uint32_t)rd(3) << 32) | (uint32_t)rd(2));
+      r[q].c = rd(4);
+      r[q].dm = rd(5);
+      r[q].w = rd(6);
+      r[q].src = rd(7);
     }
-    const u16x2 tv = {(unsigned short)tau, (unsigned short)tau};
-    const u16x2 dv = {(unsigned short)pdm[p], (unsigned short)pdm[p]};
+    int64_t src[kLevelGroup], hi[kLevelGroup];
+    bool use[kLevelGroup];
+    uint4 v0[kLevelGroup], v1[kLevelGroup];
+#pragma unroll
+    for (int q = 0; q < kLevelGroup; q++) {
+      // source cell of the group's first cell; readable cells [lo, hi)
+      src[q] = dst - rj + r[q].base;
+      hi[q] = r[q].lo + (kFront ? ws[r[q].src] : r[q].w);
+      use[q] = pg + q < p1 && Beff - r[q].c >= 0 && src[q] + kVecCells > r[q].lo && src[q] < hi[q];
+      const uint4* v = reinterpret_cast<const uint4*>(
+          m + (use[q] ? src[q] - (src[q] & (kVecCells - 1)) : dst));
+      v0[q] = v[0];
+      v1[q] = v[1];
+    }
+#pragma unroll
+    for (int q = 0; q < kLevelGroup; q++) {
+      if (!use[q]) continue;
+      const int32_t a = (int32_t)(src[q] & (kVecCells - 1));
+      const uint32_t wd[8] = {v0[q].x, v0[q].y, v0[q].z, v0[q].w,
+                              v1[q].x, v1[q].y, v1[q].z, v1[q].w};
+      uint32_t x[4];
+      switch (a) {
+        case 0: take8<0>(wd, x); break;
+        case 1: take8<1>(wd, x); break;
+        case 2: take8<2>(wd, x); break;
+        case 3: take8<3>(wd, x); break;
+        case 4: take8<4>(wd, x); break;
+        case 5: take8<5>(wd, x); break;
+        case 6: take8<6>(wd, x); break;
+        default: take8<7>(wd, x); break;
+      }
+      if (src[q] < r[q].lo || src[q] + kVecCells > hi[q]) {   // the row's edge: outside is infinite
+#pragma unroll
+        for (int c = 0; c < kVecCells; c++)
+          if (src[q] + c < r[q].lo || src[q] + c >= hi[q]) x[c / 2] |= 0xFFFFu << (16 * (c % 2));
+      }
+      // budget test of Algorithm 1: opt[L, t] + c <= B, i.e. opt[L, t] <= tau
+      const unsigned short tau = (unsigned short)(Beff - r[q].c);
+      const unsigned short dm = (unsigned short)r[q].dm;
+      const u16x2 tv = {tau, tau};
+      const u16x2 dv = {dm, dm};
+#pragma unroll
+      for (int c = 0; c < 4; c++)
+        acc[c] = __builtin_bit_cast(uint32_t, wf::relax2(__builtin_bit_cast(u16x2, acc[c]),
+                                                         __builtin_bit_cast(u16x2, x[c]), tv, dv));
+    }
+  }
+  // the waves' minima meet in LDS; wave 0 stores
+  if (wave > 0) s_acc[wave - 1][lane] = make_uint4(acc[0], acc[1], acc[2], acc[3]);
+  if (kLevelWaves > 1) __syncthreads();
+  if (wave > 0 || !live) return;
+#pragma unroll
+  for (int q = 0; q < kLevelWaves - 1; q++) {
+    const uint4 o = s_acc[q][lane];
+    const uint32_t ov[4] = {o.x, o.y, o.z, o.w};
 #pragma unroll
     for (int c = 0; c < 4; c++)
-      acc[c] = __builtin_bit_cast(uint32_t, wf::relax2(__builtin_bit_cast(u16x2, acc[c]),
-                                                       __builtin_bit_cast(u16x2, x[c]), tv, dv));
+      acc[c] = __builtin_bit_cast(uint32_t,
+                                  __builtin_elementwise_min(__builtin_bit_cast(u16x2, acc[c]),
+                                                            __builtin_bit_cast(u16x2, ov[c])));
   }
   if (t_first < 0) {                                 // cells before t = 0: padding, infinite
 #pragma unroll
@@ -203,6 +263,24 @@ __global__ __launch_bounds__(kFillThreads) void k_fill_level_vec(
       if (t_first + c < 0) acc[c / 2] |= 0xFFFFu << (16 * (c % 2));
   }
   *reinterpret_cast<uint4*>(m + dst) = make_uint4(acc[0], acc[1], acc[2], acc[3]);
+}
+
+// The level fill's record of each pair (built once per family).
+__global__ void k_level_pairs(int64_t P, const int32_t* __restrict__ pidx,
+                              const int32_t* __restrict__ pdt, const int32_t* __restrict__ pdm,
+                              const int32_t* __restrict__ pc, const int32_t* __restrict__ w,
+                              const int64_t* __restrict__ row_off, LevelPair* lp) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= P) return;
+  const int32_t i = pidx[p];
+  LevelPair r;
+  r.lo = row_off[i];
+  r.base = row_off[i] - pdt[p];
+  r.c = pc[p];
+  r.dm = pdm[p];
+  r.w = w[i];
+  r.src = i;
+  lp[p] = r;
 }
 
 // The dominance skip of Section 4.2 (last paragraph) on finished rows
@@ -496,6 +574,32 @@ hipError_t launch_solve_init(rc_solution sol, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Waves per workgroup of a level of the 16-bit level fill: enough that each
+// walks at most two groups of the level's longest pair list (1 to 16), but
+// no more than keep eight waves per SIMD busy: wide rows already fill the
+// chip with workgroups, and their levels are bound by the source reads.
+template <bool kFront>
+static void launch_level_vec(rc_family f, int64_t l, dim3 grid, int64_t lb, int32_t Beff,
+                             const int32_t* ws, uint16_t* m, hipStream_t s) {
+  const int64_t most = f->level_pairs[l];
+  const int64_t blocks = (int64_t)grid.x * grid.y;
+  const int64_t cap = 8 * 4 * (int64_t)num_cus();        // eight waves per SIMD
+  int nw = 1;
+  while (nw < 16 && (int64_t)nw * 2 * kLevelGroup < most) nw *= 2;
+  while (nw > 1 && blocks * nw > cap) nw /= 2;
+#define RCDP_LEVEL_VEC(NW)                                                                  \
+  hipLaunchKernelGGL((k_fill_level_vec<kFront, NW>), grid, dim3(NW * kWave), 0, s, lb, f->w, \
+                     f->row_off, f->pred_ptr, f->lpair, Beff, ws, m)
+  switch (nw) {
+    case 1: RCDP_LEVEL_VEC(1); break;
+    case 2: RCDP_LEVEL_VEC(2); break;
+    case 4: RCDP_LEVEL_VEC(4); break;
+    case 8: RCDP_LEVEL_VEC(8); break;
+    default: RCDP_LEVEL_VEC(16); break;
+  }
+#undef RCDP_LEVEL_VEC
+}
+
 template <class T>
 static void fill_levels(rc_solution sol, T* m, hipStream_t s) {
   rc_family f = sol->f;
@@ -506,10 +610,8 @@ static void fill_levels(rc_solution sol, T* m, hipStream_t s) {
     if (sizeof(T) == 2) {
       const int64_t tiles = (f->level_maxw[l] + kVecTile - 1) / kVecTile;
       if (tiles <= 0) continue;
-      hipLaunchKernelGGL(k_fill_level_vec, dim3((unsigned)tiles, (unsigned)(le - lb)),
-                         dim3(kFillThreads), 0, s, lb, f->w, f->row_off, f->pred_ptr, f->pidx,
-                         f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, f->w,
-                         reinterpret_cast<uint16_t*>(m));
+      launch_level_vec<false>(f, l, dim3((unsigned)tiles, (unsigned)(le - lb)), lb,
+                              (int32_t)sol->Beff, f->w, reinterpret_cast<uint16_t*>(m), s);
     } else {
       const int64_t tiles = (f->level_maxw[l] + kTile - 1) / kTile;
       if (tiles <= 0) continue;
@@ -520,16 +622,33 @@ static void fill_levels(rc_solution sol, T* m, hipStream_t s) {
   }
 }
 
+// The family's level-fill pair records, built by its first level fill.
+static hipError_t ensure_level_pairs(rc_family f, hipStream_t s) {
+  if (f->lpair || f->P == 0) return hipSuccess;
+  f->lpair = f->arena.get_n<LevelPair>(f->P + kLevelGroup);   // a group may read past the end
+  if (!f->lpair) return hipErrorOutOfMemory;
+  hipError_t e = hipMemsetAsync(f->lpair + f->P, 0, sizeof(LevelPair) * kLevelGroup, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_level_pairs, dim3((unsigned)((f->P + 255) / 256)), dim3(256), 0, s, f->P,
+                     f->pidx, f->pdt, f->pdm, f->pc, f->w, f->row_off, f->lpair);
+  return hipGetLastError();
+}
+
 hipError_t launch_fill(rc_solution sol, hipStream_t s) {
-  if (sol->cell32)
+  if (sol->cell32) {
     fill_levels(sol, sol->m32, s);
-  else
+  } else {
+    const hipError_t e = ensure_level_pairs(sol->f, s);
+    if (e != hipSuccess) return e;
     fill_levels(sol, sol->m, s);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_fill_dominance(rc_solution sol, int32_t* we, hipStream_t s) {
   rc_family f = sol->f;
+  const hipError_t le = ensure_level_pairs(f, s);
+  if (le != hipSuccess) return le;
   const int64_t L = (int64_t)f->level_ptr.size() - 1;
   int64_t most = 1;                         // segment minima of the largest level
   for (int64_t l = 0; l < L; l++)
@@ -550,9 +669,8 @@ hipError_t launch_fill_dominance(rc_solution sol, int32_t* we, hipStream_t s) {
     const int64_t lb = f->level_ptr[l], le = f->level_ptr[l + 1];
     const int64_t tiles = (f->level_maxw[l] + kVecTile - 1) / kVecTile;
     if (tiles <= 0 || le <= lb) continue;
-    hipLaunchKernelGGL(k_fill_level_vec, dim3((unsigned)tiles, (unsigned)(le - lb)),
-                       dim3(kFillThreads), 0, s, lb, f->w, f->row_off, f->pred_ptr, f->pidx,
-                       f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, (const int32_t*)we, sol->m);
+    launch_level_vec<true>(f, l, dim3((unsigned)tiles, (unsigned)(le - lb)), lb,
+                           (int32_t)sol->Beff, (const int32_t*)we, sol->m, s);
     front(lb, le - lb, f->level_maxw[l]);
   }
   return hipGetLastError();

@@ -849,33 +849,25 @@ static int choose_fill_path(rc_family f) {
   if (!f->has_records || f->F < 2) return 0;
   // the family's wavefront fill: ghost-zone blocks, or fixed blocks of kJB
   // with the split-panel fill when it can take the family
-  const int wide = f->blk_kind == kBlocksGhost ? 2 : (f->has_wide ? 3 : 1);
+  const int wave = f->blk_kind == kBlocksGhost ? 2 : (f->has_wide ? 3 : 1);
   const char* env = std::getenv("RCDP_FILL");
   if (env && std::strcmp(env, "level") == 0) return 0;
   if (env && std::strcmp(env, "wavefront") == 0 && f->blk_kind == kBlocksFixed) return 1;
-  if (env && (std::strcmp(env, "wide") == 0 || std::strcmp(env, "ghost") == 0)) return wide;
-  // the ghost-zone fill measured at least as fast as the level launches on
-  // every workload shape; the fixed-block fills pay off on tables with rows
-  // of 2^16 cells and more, and on wide tables of many levels, where one
-  // persistent launch beats one launch per level
-  if (wide == 2) return 2;
-  if (f->max_row >= 65536) {
-    // Between the split-panel wavefront and the level launches on rows of
-    // 2^16 cells and more, by their measured costs on this GPU: the
-    // wavefront runs its 256-cell columns at most three per compute unit at
-    // a time, each through every row of the table at about 2.5 us per row;
-    // a level launch over rows this wide costs about 15 us.  Tables of few
-    // levels and very long rows (the U-Net shape) take the level launches.
-    if (wide != 3) return wide;
-    const int64_t levels = (int64_t)f->level_ptr.size() - 1;
-    const int64_t slots = 3 * (int64_t)num_cus();
-    const int64_t col_rounds = (wide_columns(f) + slots - 1) / slots;
-    const double wave_us = 2.5 * (double)f->F * (double)col_rounds;
-    const double level_us = 15.0 * (double)levels;
-    return level_us < wave_us ? 0 : wide;
-  }
-  if (wide == 3 && f->F <= kGhostMaxSets) return 3;
-  return (f->max_row >= 8192 && f->level_ptr.size() > 100) ? wide : 0;
+  if (env && (std::strcmp(env, "wide") == 0 || std::strcmp(env, "ghost") == 0)) return wave;
+  if (wave == 1) return 0;
+  // The wavefront against the level launches, by their measured costs on
+  // this GPU.  The wavefront runs its 256-cell columns at most three per
+  // compute unit at a time, each through every row of the table at about
+  // 2.5 us per row.  A level launch costs about 6 us, plus the source reads
+  // of its pairs (2 bytes per relaxation) at about 4 TB/s.  Few levels of
+  // many sets or of very long rows (the ladder and U-Net shapes) take the
+  // level launches; many levels take the wavefront.
+  const int64_t levels = (int64_t)f->level_ptr.size() - 1;
+  const int64_t slots = 3 * (int64_t)num_cus();
+  const int64_t col_rounds = ((f->max_row + kWC - 1) / kWC + slots - 1) / slots;
+  const double wave_us = 2.5 * (double)f->F * (double)col_rounds;
+  const double level_us = 6.0 * (double)levels + 2.0 * (double)f->relax / 4.0e6;
+  return level_us < wave_us ? 0 : wave;
 }
 
 }  // extern "C"

@@ -100,6 +100,19 @@ struct DevStatus {
   int64_t bmin;          // smallest feasible budget (rc_min_budget)
 };
 
+// One pair (L, L') of the level fill (fill.hip): the source row's first
+// cell lo, the source cell of target cell t' of L' at base - row_off(L') + t'
+// (base = lo - dt), the budget term, the addition, the source row's width
+// and index.
+struct LevelPair {
+  int64_t lo;
+  int64_t base;
+  int32_t c;
+  int32_t dm;
+  int32_t w;
+  int32_t src;
+};
+
 // Panel / triangle records of the blocked fill (blocks.hip).
 struct BlockRecords {
   int32_t* src = nullptr;       // [R] source family index
@@ -150,6 +163,7 @@ struct rc_family_s {
   // device: predecessor pairs, CSR by target
   int64_t* pred_ptr = nullptr;    // [F+1]
   int32_t *pidx = nullptr, *pdt = nullptr, *pdm = nullptr, *pc = nullptr;
+  rcdp::LevelPair* lpair = nullptr; // [P] the level fill's pair records (built on first use)
   // blocked fill: records per block of at most kJB targets (absent when too large)
   int32_t blk_kind = 0;           // kBlocksFixed or kBlocksGhost (0: no records)
   int64_t nblk = 0;
