@@ -101,8 +101,13 @@ enum rc_status {
 };
 
 /* Family statistics (rc_family_info).
- *  relaxations: the DP's unit of work, sum over predecessor pairs (L, L')
- *  of w_L = T(L \ boundary(L)) + 1, the cells of row L that can be finite.
+ *  relaxations: the DP's unit of work, one (L, L', t) of Algorithm 1's
+ *  update loop (Appendix A) whose source opt[L, t] can be finite: the sum
+ *  over predecessor pairs (L, L') of w_L = T(L \ boundary(L)) + 1, since a
+ *  chain ending at L recomputes only nodes of L \ boundary(L) (Eq. 1
+ *  charges V_i \ boundary(L_i) per segment), so opt[L, t] is infinite for
+ *  larger t.  Section 4.2's complexity O(T(V) #F^2) counts the same loop
+ *  over every t.
  *  table_cells: sum over the family of w_L. */
 typedef struct {
   int32_t n;            /* nodes */
