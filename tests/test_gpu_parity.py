@@ -13,6 +13,8 @@ import pytest
 
 from paper_1905_11722_amd import workloads as W
 
+from tests.closed_forms import antichain_pruned_expected
+
 pytestmark = pytest.mark.gpu
 
 
@@ -107,6 +109,45 @@ def test_antichain_wide_levels(rc, oracle_mod):
     g = W.antichain(9, seed=4, tmax=30, mmax=20)
     for B in (2 * max(g.M), sum(g.M), 2 * sum(g.M)):
         compare(rc, oracle_mod, g, "exact", B)
+
+
+@pytest.mark.parametrize("path", ["level", "wavefront", "wide"])
+def test_node_limit_antichain(rc, monkeypatch, path):
+    """4096 nodes (64 words per set): the pruned family of an antichain, 4098
+    sets (beyond the ghost-zone fill and the traceback's LDS arrays), whole
+    table, t* and schedule against the closed form above, for both
+    objectives, at the unconstrained budget, at one where only a two-segment
+    chain fits, and at an infeasible one."""
+    monkeypatch.setenv("RCDP_FILL", path)
+    g = W.antichain(4096, seed=5, tmax=1, mmax=5)
+    n, MV, TV = g.n, sum(g.M), sum(g.T)
+    fam = rc.Graph.create(g).build_family("pruned")
+    assert fam.info["num_sets"] == n + 2 and fam.info["num_pairs"] == 2 * n + 1
+    big = max(g.M)
+    for B in (2 * MV, 2 * (MV - big), 2 * (MV - big) - 1):
+        em, ea, chain = antichain_pruned_expected(g, B)
+        for objective in ("tc", "mc"):
+            sol = fam.solve(B, objective)
+            if chain is None:
+                assert sol.status == rc.INFEASIBLE
+            else:
+                assert (sol.t_star, sol.m_star) == (TV, 0)
+                sched = sol.reconstruct()
+                assert sched.chain.tolist() == chain
+                assert (sched.overhead, sched.cache_mem) == (TV, 0)
+                assert not sched.cached.any()
+                seg = np.full(n, len(chain) - 1)
+                if len(chain) == 2:
+                    seg[chain[0] - 1] = 0
+                    assert sched.peak == max(2 * big, 2 * (MV - big))
+                else:
+                    assert sched.peak == 2 * MV
+                np.testing.assert_array_equal(sched.seg, seg)
+            if objective == "tc":
+                m, a = sol.table()
+                np.testing.assert_array_equal(m, em, err_msg=f"B={B}")
+                np.testing.assert_array_equal(a, ea, err_msg=f"B={B}")
+            sol.free()
 
 
 def test_empty_and_single(rc, oracle_mod):

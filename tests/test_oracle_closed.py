@@ -116,3 +116,26 @@ def test_family_exceeds_cap(oracle_mod):
     r = oracle_mod.solve(g, "exact", 10 ** 6, max_sets=255)
     assert r.status == oracle_mod.E_TOO_MANY_SETS
     assert oracle_mod.solve(g, "exact", 10 ** 6, max_sets=256).num_sets == 256
+
+
+@pytest.mark.parametrize("n,seed", [(2, 0), (5, 1), (12, 2), (30, 3)])
+def test_antichain_pruned_closed_form(oracle_mod, n, seed):
+    """The closed form the GPU tests use at the node limit (pruned family of
+    an antichain: every boundary empty, nothing cached, the one-segment chain
+    or empty -> {v} -> V) equals the oracle's whole table and traced chain at
+    the unconstrained budget, at one where only a two-segment chain fits, and
+    at an infeasible one."""
+    from tests.closed_forms import antichain_pruned_expected
+    g = W.antichain(n, seed=seed, tmax=3, mmax=5)
+    MV, big = sum(g.M), max(g.M)
+    budgets = [2 * MV, 2 * (MV - big), 2 * (MV - big) - 1, 2 * big - 1]
+    for B in [b for b in budgets if b >= 0]:
+        em, ea, chain = antichain_pruned_expected(g, B)
+        r = oracle_mod.solve(g, "pruned", B, "tc")
+        m, a = r.table()
+        np.testing.assert_array_equal(m, em, err_msg=f"n={n} B={B}")
+        np.testing.assert_array_equal(a, ea, err_msg=f"n={n} B={B}")
+        if chain is None:
+            assert r.status == oracle_mod.INFEASIBLE
+        else:
+            assert list(r.schedule()[0]) == chain
