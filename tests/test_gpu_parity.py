@@ -150,6 +150,39 @@ def test_node_limit_antichain(rc, monkeypatch, path):
             sol.free()
 
 
+@pytest.mark.parametrize("path", ["level", "wide"])
+def test_node_limit_chain(rc, monkeypatch, path):
+    """A 4096-node chain with unit costs at an unconstrained budget: the
+    pruned family is every prefix (4097 sets, 8.4 M pairs, 1.1e10
+    relaxations).  A prefix's boundary is its last node, so caching every
+    node but the sink takes all 4096 prefixes as the chain (the traceback at
+    its longest) for the least overhead, 1 = T(sink) (reading 8's floor,
+    cache memory n - 1, peak n + 1 in the last segment); overhead t needs
+    n - t cached nodes, so row V is opt[V, t] = n - t for t >= 1; the
+    memory-centric optimum is the one-segment chain (t = n, m = 0)."""
+    monkeypatch.setenv("RCDP_FILL", path)
+    n = 4096
+    g = W.Graph(n, [[v + 1] if v + 1 < n else [] for v in range(n)], [1] * n, [1] * n)
+    fam = rc.Graph.create(g).build_family("pruned")
+    assert fam.info["num_sets"] == n + 1 and fam.info["num_pairs"] == n * (n + 1) // 2
+    B = 2 * n
+    sol = fam.solve(B, "tc")
+    assert (sol.t_star, sol.m_star) == (1, n - 1)
+    sched = sol.reconstruct()
+    assert sched.chain.tolist() == list(range(1, n + 1))
+    np.testing.assert_array_equal(sched.seg, np.arange(n))
+    assert sched.cached.tolist() == [True] * (n - 1) + [False]
+    assert (sched.overhead, sched.peak, sched.cache_mem) == (1, n + 1, n - 1)
+    m, _ = sol.table(first=n, count=1)
+    np.testing.assert_array_equal(m[0], np.array([-1] + [n - t for t in range(1, n + 1)]))
+    sol.free()
+    sol = fam.solve(B, "mc")
+    assert (sol.t_star, sol.m_star) == (n, 0)
+    sched = sol.reconstruct()
+    assert sched.chain.tolist() == [n] and sched.overhead == n and sched.peak == 2 * n
+    sol.free()
+
+
 def test_empty_and_single(rc, oracle_mod):
     g0 = W.Graph(0, [], [], [])
     for mode in ("exact", "pruned"):

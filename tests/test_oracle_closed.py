@@ -139,3 +139,24 @@ def test_antichain_pruned_closed_form(oracle_mod, n, seed):
             assert r.status == oracle_mod.INFEASIBLE
         else:
             assert list(r.schedule()[0]) == chain
+
+
+@pytest.mark.parametrize("n", [2, 5, 8, 20])
+def test_unit_chain_closed_form(oracle_mod, n):
+    """The closed form the GPU tests use for a 4096-node chain with unit
+    costs at an unconstrained budget: least overhead 1 with every node but
+    the sink cached (all n prefixes as the chain, peak n + 1), row V
+    opt[V, t] = n - t for t >= 1, and the memory-centric optimum the
+    one-segment chain (t = n, m = 0, peak 2 n)."""
+    g = W.Graph(n, [[v + 1] if v + 1 < n else [] for v in range(n)], [1] * n, [1] * n)
+    r = oracle_mod.solve(g, "pruned", 2 * n, "tc")
+    assert (r.num_sets, r.num_pairs) == (n + 1, n * (n + 1) // 2)
+    assert (r.t_star, r.m_star, r.overhead, r.peak, r.cache_mem) == (1, n - 1, 1, n + 1, n - 1)
+    chain, seg, cached = r.schedule()
+    assert list(chain) == list(range(1, n + 1)) and list(seg) == list(range(n))
+    assert list(cached) == [True] * (n - 1) + [False]
+    m, _ = r.table()
+    assert m[n].tolist() == [-1] + [n - t for t in range(1, n + 1)]
+    r = oracle_mod.solve(g, "pruned", 2 * n, "mc")
+    assert (r.t_star, r.m_star, r.overhead, r.peak) == (n, 0, n, 2 * n)
+    assert list(r.schedule()[0]) == [n]
