@@ -122,3 +122,32 @@ def test_wide_levels_exact_antichain(rc):
             assert (t, m) == (sol.t_star, sol.m_star), (B, objective)
             sol.free()
             assert (sched.overhead, sched.cache_mem) == (t, m) and sched.peak <= B
+
+
+def test_node_limit(rc):
+    """4096 nodes: the memory-indexed solve of a unit-cost chain (4097 sets,
+    a 4096-step traceback) and of an antichain, against the closed forms
+    pinned in test_oracle_closed.py: the chain's least overhead 1 with n - 1
+    cached nodes and every prefix as the chain, its memory-centric optimum
+    the one-segment chain; the antichain's T(V) at no cached memory."""
+    from tests.closed_forms import antichain_pruned_expected
+    n = 4096
+    g = W.Graph(n, [[v + 1] if v + 1 < n else [] for v in range(n)], [1] * n, [1] * n)
+    fam = rc.Graph.create(g).build_family("pruned")
+    t, m, _, sched = fam.solve_dual(2 * n, "tc", schedule=True)
+    assert (t, m) == (1, n - 1)
+    assert sched.chain.tolist() == list(range(1, n + 1))
+    assert (sched.overhead, sched.peak, sched.cache_mem) == (1, n + 1, n - 1)
+    t, m, _, sched = fam.solve_dual(2 * n, "mc", schedule=True)
+    assert (t, m) == (n, 0) and sched.chain.tolist() == [n]
+    g = W.antichain(n, seed=5, tmax=1, mmax=5)
+    fam = rc.Graph.create(g).build_family("pruned")
+    MV, big = sum(g.M), max(g.M)
+    for B in (2 * MV, 2 * (MV - big), 2 * (MV - big) - 1):
+        _, _, chain = antichain_pruned_expected(g, B)
+        t, m, _, sched = fam.solve_dual(B, "tc", schedule=True)
+        if chain is None:
+            assert (t, m) == (-1, -1)
+        else:
+            assert (t, m) == (sum(g.T), 0)
+            assert sched.overhead == sum(g.T) and sched.cache_mem == 0 and sched.peak <= B
