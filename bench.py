@@ -86,9 +86,10 @@ def run_step(rcdp, g, case):
     kernel = sol.fill_kernel()
     info = fam.info
     t_star = sol.t_star
+    m_star = sol.m_star
     sol.free()
     fam.free()
-    return info, fill_ms, kernel_ms, t_star, sched, kernel
+    return info, fill_ms, kernel_ms, (t_star, m_star), sched, kernel
 
 
 def time_phases(rcdp, torch, case, steps):
@@ -126,7 +127,7 @@ def time_case(rcdp, torch, case, steps, warmup):
     fills, kernels = [], []
     t0 = time.perf_counter()
     for _ in range(steps):
-        info, fill_ms, kernel_ms, t_star, sched, kernel = run_step(rcdp, g, case)
+        info, fill_ms, kernel_ms, (t_star, m_star), sched, kernel = run_step(rcdp, g, case)
         fills.append(fill_ms)
         kernels.append(kernel_ms)
     torch.cuda.synchronize()
@@ -144,6 +145,8 @@ def time_case(rcdp, torch, case, steps, warmup):
         "kernel_ms_max": max(kernels),
         "info": info,
         "t_star": t_star,
+        "m_star": m_star,
+        "schedule": sched,
         "k": None if sched is None else int(len(sched.chain)),
         "kernel": kernel,
     }
@@ -175,15 +178,19 @@ def mc_sweep(rcdp, torch, name="resnet50", count=32, reps=2):
         for _, sol in sols:
             sol.free()
         t3 = time.perf_counter()
+        fills = []
         for B in budgets:
             sol = fam.solve(B, "mc")
             sol.reconstruct()
+            fills.append(round(sol.fill_ms(), 4))
             sol.free()
         torch.cuda.synchronize()
         t4 = time.perf_counter()
         res = {"workload": name, "budgets": count, "B_min": b_min, "B_max": top,
                "min_budget_ms": (t1 - t0) * 1e3, "batched_sweep_ms": (t2 - t1) * 1e3,
-               "batched_fill_ms": batch_fill, "one_by_one_ms": (t4 - t3) * 1e3,
+               "batched_fill_ms": batch_fill,
+               "batched_fill_per_budget_ms": batch_fill / count,
+               "one_by_one_ms": (t4 - t3) * 1e3, "one_by_one_fill_ms": fills,
                "t_mc_first_last": [t_mc[0], t_mc[-1]]}
         if best is None or res["batched_sweep_ms"] < best["batched_sweep_ms"]:
             best = res
@@ -301,16 +308,28 @@ def cpu_baseline(case, relaxations):
     (tests/test_oracle_parallel.py)."""
     from oracle import oracle
     legs = {}
+    ref = None
     for parallel in (True, False):
-        t0 = time.perf_counter()
-        r = oracle.solve(case.graph, case.mode, case.B, case.objective, parallel=parallel)
-        dt = time.perf_counter() - t0
+        # the single-threaded leg runs pinned to one core of the allowed set
+        keep = os.sched_getaffinity(0) if hasattr(os, "sched_getaffinity") else None
+        if not parallel and keep:
+            os.sched_setaffinity(0, {min(keep)})
+        try:
+            t0 = time.perf_counter()
+            r = oracle.solve(case.graph, case.mode, case.B, case.objective, parallel=parallel)
+            dt = time.perf_counter() - t0
+        finally:
+            if not parallel and keep:
+                os.sched_setaffinity(0, keep)
         legs[parallel] = (dt, r.t_star, r.num_sets, oracle.threads(parallel))
-        del r
+        if parallel:
+            ref = r
+        else:
+            del r
     dt, t_star, num_sets, cores = legs[True]
     dt1, t_star1, _, _ = legs[False]
     assert t_star1 == t_star
-    return {
+    return ref, {
         "value": relaxations / dt,
         "unit": "relaxations/s",
         "cores": cores,
@@ -320,9 +339,28 @@ def cpu_baseline(case, relaxations):
                    f"OpenMP build on {cores} threads, {dt:.2f} s; t*={t_star}"),
         "seconds": dt,
         "t_star": t_star,
-        "one_core": {"value": relaxations / dt1, "seconds": dt1, "cores": 1},
+        "one_core": {"value": relaxations / dt1, "seconds": dt1, "cores": 1,
+                     "pinned": hasattr(os, "sched_setaffinity")},
         "host": host_description(),
     }
+
+
+def same_run_parity(ref, res):
+    """The GPU's last timed step against the oracle's solve of the same
+    workload in this run: t*, opt[V, t*], the traced chain, seg, cached and
+    the Eq. 1 / Eq. 2 re-evaluation (the whole tables are compared in the GPU
+    tests)."""
+    out = {"t_star": res["t_star"] == ref.t_star, "m_star": res["m_star"] == ref.m_star}
+    sched = res["schedule"]
+    if sched is not None and ref.t_star >= 0:
+        chain, seg, cached = ref.schedule()
+        out["chain"] = list(map(int, sched.chain)) == list(map(int, chain))
+        out["seg"] = list(map(int, sched.seg)) == list(map(int, seg))
+        out["cached"] = list(map(bool, sched.cached)) == list(map(bool, cached))
+        out["overhead_peak_cache"] = (sched.overhead, sched.peak, sched.cache_mem) == (
+            ref.overhead, ref.peak, ref.cache_mem)
+    out["all_equal"] = all(out.values())
+    return out
 
 
 def measured_peaks(torch, copy_bytes=2 << 30):
@@ -512,8 +550,9 @@ def main():
         "dominance": dominance,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(case, W)
-        assert out["cpu_baseline"]["t_star"] == main_res["t_star"], "oracle and GPU disagree on t*"
+        ref, out["cpu_baseline"] = cpu_baseline(case, W)
+        out["parity"] = same_run_parity(ref, main_res)
+        assert out["parity"]["all_equal"], f"oracle and GPU disagree: {out['parity']}"
     print(json.dumps(out), flush=True)
 
 
