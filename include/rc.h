@@ -58,6 +58,12 @@
  *    (default from the table's width).
  *  - RCDP_DEBUG (any value): the wavefront fills print their launch shape
  *    to stderr.
+ *  - RCDP_TRACE = scan | slice: the traceback of rc_reconstruct (see
+ *    rc_solution_trace_path).  Unset: the slice when its (t* + 1) P pair
+ *    tests (P the family's pairs) number at most 2^26 and at most 4e5 per
+ *    step of the longest possible chain (min(num_sets - 1, n) steps), and
+ *    its 4 (t* + 1) num_sets bytes at most 64 MiB; slice forces it within
+ *    that size.
  *  - RCDP_JITTER = n (a nonzero integer): the race test.  The persistent
  *    wavefront fills (k_fill_blocked, k_fill_wide, k_fill_ghost) make their
  *    waves sleep pseudo-random times drawn from n at block starts and
@@ -300,6 +306,13 @@ int rc_solution_fill_kernel_ms(rc_solution s, float* ms);
  * sets on 32-bit cells (k_fill_level).  Returns RC_OK or RC_E_ARG (NULL
  * argument). */
 int rc_solution_fill_path(rc_solution s, int32_t* path);
+/* Which traceback the last rc_reconstruct of the handle ran (both follow
+ * the optarg rule of Section 4.2 and give the same chain): *path = 0 a
+ * scan of the predecessor list at every step (k_trace), 1 optarg of every
+ * cell (L', t') with t' <= t* evaluated at once, then followed
+ * (k_trace_args, k_trace_follow); -1 before the first rc_reconstruct.
+ * Returns RC_OK or RC_E_ARG (NULL argument). */
+int rc_solution_trace_path(rc_solution s, int32_t* path);
 
 /*
  * rc_reconstruct -- trace optarg back from (V, t*) (Section 4.2) and

@@ -23,6 +23,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdlib>
+#include <cstring>
 
 #include "rc_internal.h"
 #include "dominance.h"
@@ -561,6 +563,156 @@ __global__ __launch_bounds__(kTraceThreads) void k_trace(
                                   cached, s_chain, s_M);
 }
 
+// The traceback through an optarg slice.  When t* is small, every step of
+// the walk stays among the cells (L', t') with t' <= t*: optarg of all of
+// them (by the rule of k_trace) is evaluated at once, over the whole chip,
+// and the walk then follows it, one load per step instead of a scan of the
+// predecessor list.  k_trace_args: workgroup (x, L') takes the 64 cells
+// t' = 64 x + lane of row L', its waves the predecessor list in interleaved
+// groups of 64 pairs (group g to wave g mod kArgWaves).  Each lane keeps the
+// first hit of its wave, and the least over the waves is the first hit of
+// the list.  A wave stops when every lane has a hit: its later groups hold
+// only larger indices.  The result of cell (L', t') is nxt[L' S + t'] =
+// L | (t' - dt) << 16 (S = t* + 1 <= 65536, family indices below 65535), or
+// kNoNext: no hit, infinite, L' empty or t' beyond the row.
+constexpr int kArgWaves = 4;
+constexpr uint32_t kNoNext = 0xFFFFFFFFu;
+
+template <class Cell>
+__global__ __launch_bounds__(kArgWaves* kWave) void k_trace_args(
+    int32_t S, const int32_t* __restrict__ w, const int64_t* __restrict__ row_off,
+    const int64_t* __restrict__ pred_ptr, const int32_t* __restrict__ pidx,
+    const int32_t* __restrict__ pdt, const int32_t* __restrict__ pdm,
+    const int32_t* __restrict__ pc, int32_t Beff, const Cell* __restrict__ m,
+    uint32_t* __restrict__ nxt) {
+  __shared__ int32_t s_hit[kArgWaves][kWave];
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const int64_t j = blockIdx.y;
+  const int32_t t = blockIdx.x * kWave + lane;
+  const int32_t wj = w[j];
+  const uint32_t mj = m[row_off[j] + (t < wj ? t : 0)];
+  const bool need = j > 0 && t < S && t < wj && mj != cell_inf<Cell>();
+  const int64_t p0 = pred_ptr[j], p1 = pred_ptr[j + 1];
+  int32_t hit = INT32_MAX;
+  if (__any(need)) {
+    for (int64_t g = p0 + (int64_t)wave * kWave; g < p1; g += kArgWaves * kWave) {
+      // lane l holds pair g + l: the source row's cell of target t at
+      // base + t, in the row when t - dt lies in [0, w_L); past the list w = 0
+      const int64_t p = g + lane;
+      const int64_t pq = p < p1 ? p : p0;
+      const int32_t i = pidx[pq], dt = pdt[pq], c = pc[pq], dm = pdm[pq];
+      const int64_t base = row_off[i] - dt;
+      const int32_t wi = p < p1 ? w[i] : 0;
+      const uint32_t blo = (uint32_t)base, bhi = (uint32_t)((uint64_t)base >> 32);
+      const int32_t cnt = (int32_t)std::min<int64_t>(kWave, p1 - g);
+      for (int32_t k0 = 0; k0 < cnt; k0 += 8) {
+        // eight source cells loaded before any test (a cell outside its row
+        // is read at the row's first cell and not used)
+        uint32_t x[8];
+        bool in[8];
+#pragma unroll
+        for (int u = 0; u < 8; u++) {
+          const int k = k0 + u;
+          const int32_t dtk = __builtin_amdgcn_readlane(dt, k);
+          const int32_t wk = __builtin_amdgcn_readlane(wi, k);
+          const int64_t bk = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(bhi, k) << 32) |
+                                       (uint32_t)__builtin_amdgcn_readlane(blo, k));
+          in[u] = (uint32_t)(t - dtk) < (uint32_t)wk;
+          x[u] = m[bk + (in[u] ? t : dtk)];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; u++) {
+          const int k = k0 + u;
+          const int32_t ck = __builtin_amdgcn_readlane(c, k);
+          const int32_t dmk = __builtin_amdgcn_readlane(dm, k);
+          if (hit == INT32_MAX && in[u] && x[u] != cell_inf<Cell>() &&
+              (int64_t)x[u] <= (int64_t)Beff - ck && (uint32_t)(x[u] + dmk) == mj)
+            hit = (int32_t)(g - p0) + k;
+        }
+      }
+      if (!__any(need && hit == INT32_MAX)) break;
+    }
+  }
+  s_hit[wave][lane] = need ? hit : INT32_MAX;
+  __syncthreads();
+  if (wave != 0 || t >= S) return;
+  int32_t h = INT32_MAX;
+#pragma unroll
+  for (int q = 0; q < kArgWaves; q++) h = min(h, s_hit[q][lane]);
+  uint32_t e = kNoNext;
+  if (h != INT32_MAX) {
+    const int64_t p = p0 + h;
+    e = (uint32_t)pidx[p] | ((uint32_t)(t - pdt[p]) << 16);
+  }
+  nxt[j * S + t] = e;
+}
+
+// The walk over the slice of k_trace_args from (V, t*), then Eq. 1 and
+// Eq. 2 of the chain as in k_trace.  Thread 0 walks; the other waves first
+// read the slice from its last row down (the order of the walk), so that
+// the walk's loads find it in this compute unit's L2.
+__global__ __launch_bounds__(kTraceThreads) void k_trace_follow(
+    int64_t F, int n, int words, int64_t fstride, const uint64_t* __restrict__ bits,
+    const uint64_t* __restrict__ bd, const int32_t* __restrict__ A, const int32_t* __restrict__ T,
+    const int32_t* __restrict__ M, int32_t S, const uint32_t* __restrict__ nxt, int64_t T_total,
+    DevStatus* st, int32_t* chain, int32_t* seg, uint8_t* cached) {
+  __shared__ int32_t s_chain[kMaxNodes + 1];
+  __shared__ int32_t s_M[kMaxNodes];
+  __shared__ int32_t s_k;
+  const int tid = threadIdx.x;
+  if (tid >= kWave) {
+    // eight loads in flight per lane
+    constexpr int64_t kStride = kTraceThreads - kWave;
+    const uint4* q = reinterpret_cast<const uint4*>(nxt);
+    uint32_t acc = 0;
+    int64_t x = F * S / 4 - 1 - (tid - kWave);
+    for (; x >= 7 * kStride; x -= 8 * kStride) {
+      uint4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; u++) v[u] = q[x - u * kStride];
+#pragma unroll
+      for (int u = 0; u < 8; u++) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+    }
+    for (; x >= 0; x -= kStride) {
+      const uint4 v = q[x];
+      acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+    if (acc == 0x7fffffffu) st->pad0 = (int32_t)acc;   // keeps the loads
+  } else if (tid == 0) {
+    int64_t j = F - 1;
+    int32_t t = st->t_sel;
+    int32_t k = 0;
+    bool bad = t < 0 || t >= S;
+    while (!bad && j != 0) {
+      if (k >= F || k > n) {                      // each step removes a node
+        bad = true;
+        break;
+      }
+      const uint32_t e = nxt[j * S + t];
+      if (e == kNoNext) {
+        bad = true;
+        break;
+      }
+      chain[k++] = (int32_t)j;
+      j = e & 0xFFFFu;
+      t = (int32_t)(e >> 16);
+    }
+    if (t != 0) bad = true;                        // the walk must end at (empty, 0)
+    s_k = bad ? -1 : k;
+  }
+  __syncthreads();
+  const int32_t k = s_k;
+  if (k < 0) {
+    if (tid == 0) {
+      st->error = 2;
+      st->k = -1;
+    }
+    return;
+  }
+  finish_schedule<kTraceThreads>(k, n, words, fstride, bits, bd, A, T, M, T_total, st, chain, seg,
+                                  cached, s_chain, s_M);
+}
+
 }  // namespace
 
 hipError_t launch_solve_init(rc_solution sol, hipStream_t s) {
@@ -696,29 +848,64 @@ hipError_t launch_select(rc_solution sol, hipStream_t s) {
   return hipGetLastError();
 }
 
+// The slice traceback is taken when its evaluation, about (t* + 1) P pair
+// tests spread over the chip, costs less than the longest walk the scan
+// could take, and its slice of 4 (t* + 1) F bytes is small; otherwise the
+// scan of k_trace.  Measured here: a scan step costs about 0.8 us, the
+// slice's tests run at about 5e11 per second (so 4e5 tests per step of the
+// longest chain, min(F - 1, n) steps), and its walk costs about 0.2 us a
+// step.  RCDP_TRACE = scan | slice forces one (slice within its size limits).
+constexpr int64_t kSliceTests = (int64_t)1 << 26;
+constexpr int64_t kSliceTestsPerStep = 400000;
+constexpr int64_t kSliceCells = (int64_t)1 << 24;
+
+static bool use_slice(rc_solution sol) {
+  rc_family f = sol->f;
+  const int64_t S = sol->t_star + 1;
+  if (sol->t_star < 0 || S > 65536 || f->F >= 65535 || f->F * S > kSliceCells) return false;
+  const char* env = std::getenv("RCDP_TRACE");
+  if (env && std::strcmp(env, "scan") == 0) return false;
+  if (env && std::strcmp(env, "slice") == 0) return true;
+  const int64_t steps = std::min<int64_t>(f->F - 1, f->g->n);
+  return S * f->P <= std::min<int64_t>(kSliceTests, kSliceTestsPerStep * steps);
+}
+
 template <class T>
-static void trace_t(rc_solution sol, const T* m, hipStream_t s) {
+static hipError_t trace_t(rc_solution sol, const T* m, hipStream_t s) {
   rc_family f = sol->f;
   rc_graph g = f->g;
-  if (f->F <= kTraceLds)
+  sol->trace_path = use_slice(sol) ? 1 : 0;
+  if (sol->trace_path == 1) {
+    const int32_t S = (int32_t)(sol->t_star + 1);
+    const int64_t cells = f->F * (int64_t)S;
+    if (sol->nxt_cells < cells) {
+      sol->nxt = sol->arena.get_n<uint32_t>(cells);
+      if (!sol->nxt) return hipErrorOutOfMemory;
+      sol->nxt_cells = cells;
+    }
+    hipLaunchKernelGGL(k_trace_args<T>, dim3((unsigned)((S + kWave - 1) / kWave), (unsigned)f->F),
+                       dim3(kArgWaves * kWave), 0, s, S, f->w, f->row_off, f->pred_ptr, f->pidx,
+                       f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, m, sol->nxt);
+    hipLaunchKernelGGL(k_trace_follow, dim3(1), dim3(kTraceThreads), 0, s, f->F, g->n, g->words,
+                       f->fstride, f->bits, f->bd, f->A, g->dT, g->dM, S, sol->nxt, g->T_total,
+                       sol->status, sol->chain, sol->seg, sol->cached);
+  } else if (f->F <= kTraceLds) {
     hipLaunchKernelGGL((k_trace<true, T>), dim3(1), dim3(kTraceThreads), 0, s, f->F, g->n, g->words,
                        f->fstride, f->bits, f->bd, f->A, g->dT, g->dM, f->w, f->row_off,
                        f->pred_ptr, f->pidx, f->pdt, f->pdm, f->pc, (int32_t)sol->Beff, m,
                        g->T_total, sol->status, sol->chain, sol->seg, sol->cached);
-  else
+  } else {
     hipLaunchKernelGGL((k_trace<false, T>), dim3(1), dim3(kTraceThreads), 0, s, f->F, g->n,
                        g->words, f->fstride, f->bits, f->bd, f->A, g->dT, g->dM, f->w,
                        f->row_off, f->pred_ptr, f->pidx, f->pdt, f->pdm, f->pc,
                        (int32_t)sol->Beff, m, g->T_total, sol->status, sol->chain, sol->seg,
                        sol->cached);
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_trace(rc_solution sol, hipStream_t s) {
-  if (sol->cell32)
-    trace_t<uint32_t>(sol, sol->m32, s);
-  else
-    trace_t<uint16_t>(sol, sol->m, s);
-  return hipGetLastError();
+  return sol->cell32 ? trace_t<uint32_t>(sol, sol->m32, s) : trace_t<uint16_t>(sol, sol->m, s);
 }
 
 template <class T>

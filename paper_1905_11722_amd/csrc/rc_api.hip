@@ -1167,6 +1167,12 @@ int rc_solution_fill_path(rc_solution s, int32_t* path) {
   return RC_OK;
 }
 
+int rc_solution_trace_path(rc_solution s, int32_t* path) {
+  if (!s || !path) return RC_E_ARG;
+  *path = s->trace_path;
+  return RC_OK;
+}
+
 int rc_reconstruct(rc_solution sol, void* stream, int32_t* k, int32_t* chain_host,
                    int32_t* seg_host, uint8_t* cached_host, int64_t* overhead, int64_t* peak,
                    int64_t* cache_mem) {
@@ -1183,7 +1189,12 @@ int rc_reconstruct(rc_solution sol, void* stream, int32_t* k, int32_t* chain_hos
   Staging stage(lay.bytes);
   if (!sol->pack) sol->pack = sol->arena.get(lay.bytes);
   if (!stage.data() || !sol->pack) return RC_E_NOMEM;
-  RC_HIP(launch_trace(sol, s));
+  const hipError_t te = launch_trace(sol, s);
+  if (te == hipErrorOutOfMemory) return RC_E_NOMEM;
+  if (te != hipSuccess) {
+    set_last_error("traceback launch", te);
+    return RC_E_DEVICE;
+  }
   PackList PL;
   PL.add(sol->status, sizeof(DevStatus), (int64_t)o_st);
   PL.add(sol->chain, sizeof(int32_t) * kmax, (int64_t)o_ch);

@@ -206,6 +206,9 @@ struct rc_solution_s {
   int32_t* seg = nullptr;         // [n]
   uint8_t* cached = nullptr;      // [n]
   void* pack = nullptr;           // the traceback's results gathered for one copy to the host
+  uint32_t* nxt = nullptr;        // the traceback's optarg slice [F * (t* + 1)] (fill.hip)
+  int64_t nxt_cells = 0;
+  int32_t trace_path = -1;        // the last traceback: 0 predecessor scans, 1 optarg slice
   int32_t* progress = nullptr;    // blocked fill: rows finished per column
   int32_t* ticket = nullptr;      // blocked fill: next column to take
   int32_t* crec = nullptr;        // blocked fill: compact live records [clu_total * kRecInts]

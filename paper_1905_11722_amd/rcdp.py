@@ -109,6 +109,8 @@ def load_library():
     lib.rc_solution_fill_kernel_ms.argtypes = [P, ctypes.POINTER(ctypes.c_float)]
     lib.rc_solution_fill_path.restype = ctypes.c_int
     lib.rc_solution_fill_path.argtypes = [P, ctypes.POINTER(ctypes.c_int32)]
+    lib.rc_solution_trace_path.restype = ctypes.c_int
+    lib.rc_solution_trace_path.argtypes = [P, ctypes.POINTER(ctypes.c_int32)]
     lib.rc_reconstruct.restype = ctypes.c_int
     lib.rc_reconstruct.argtypes = [P, P, ctypes.POINTER(i32), P, P, P, ctypes.POINTER(i64),
                                    ctypes.POINTER(i64), ctypes.POINTER(i64)]
@@ -398,6 +400,16 @@ class Solution:
         _check(load_library().rc_solution_fill_path(self._h, ctypes.byref(path)),
                "rc_solution_fill_path")
         return self.FILL_KERNELS[path.value]
+
+    TRACE_KERNELS = ("k_trace", "k_trace_follow")
+
+    def trace_kernel(self):
+        """Name of the traceback kernel the last reconstruct ran, or None
+        before the first (see rc_solution_trace_path)."""
+        path = ctypes.c_int32()
+        _check(load_library().rc_solution_trace_path(self._h, ctypes.byref(path)),
+               "rc_solution_trace_path")
+        return self.TRACE_KERNELS[path.value] if path.value >= 0 else None
 
     def reconstruct(self):
         lib = load_library()

@@ -16,6 +16,7 @@ import pytest
 
 from oracle import oracle as O
 from paper_1905_11722_amd import workloads as W
+from tests.trace_paths import reconstruct_each
 
 pytestmark = pytest.mark.gpu
 
@@ -51,12 +52,13 @@ def compare(rc, g, mode, B, parallel=False):
         assert sol.status == rc.INFEASIBLE and (sol.t_star, sol.m_star) == (-1, -1)
     else:
         assert (sol.t_star, sol.m_star) == (ref.t_star, ref.m_star)
-        sched = sol.reconstruct()
         chain, seg, cached = ref.schedule()
-        np.testing.assert_array_equal(sched.chain, chain)
-        np.testing.assert_array_equal(sched.seg, seg)
-        np.testing.assert_array_equal(sched.cached, cached)
-        assert (sched.overhead, sched.peak, sched.cache_mem) == (ref.overhead, ref.peak, ref.cache_mem)
+        for sched in reconstruct_each(sol, ref.num_sets):
+            np.testing.assert_array_equal(sched.chain, chain)
+            np.testing.assert_array_equal(sched.seg, seg)
+            np.testing.assert_array_equal(sched.cached, cached)
+            assert (sched.overhead, sched.peak, sched.cache_mem) == (
+                ref.overhead, ref.peak, ref.cache_mem)
     m, a = sol.table()
     rm, ra = ref.table()
     want, keep = front(rm)

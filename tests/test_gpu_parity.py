@@ -5,7 +5,8 @@ rc_build_family, rc_solve, rc_reconstruct, rc_export_table) and the C
 oracle on the same seeded input, and compares: the family (members and
 order), the whole opt / optarg table over t = 0..T(V), t* and opt[V, t*]
 for both objectives, the traced chain, seg / cached, and the Eq. 1 / Eq. 2
-re-evaluation of the schedule.
+re-evaluation of the schedule, from each traceback (predecessor scans,
+optarg slice) forced in turn.
 """
 
 import numpy as np
@@ -14,6 +15,7 @@ import pytest
 from paper_1905_11722_amd import workloads as W
 
 from tests.closed_forms import antichain_pruned_expected
+from tests.trace_paths import reconstruct_each
 
 pytestmark = pytest.mark.gpu
 
@@ -45,13 +47,13 @@ def compare(rc, O, g, mode, B, objectives=("tc", "mc"), table=True, parallel=Fal
         else:
             assert sol.status == rc.OK
             assert (sol.t_star, sol.m_star) == (ref.t_star, ref.m_star)
-            sched = sol.reconstruct()
             chain, seg, cached = ref.schedule()
-            np.testing.assert_array_equal(sched.chain, chain)
-            np.testing.assert_array_equal(sched.seg, seg)
-            np.testing.assert_array_equal(sched.cached, cached)
-            assert (sched.overhead, sched.peak, sched.cache_mem) == (
-                ref.overhead, ref.peak, ref.cache_mem)
+            for sched in reconstruct_each(sol, ref.num_sets):
+                np.testing.assert_array_equal(sched.chain, chain)
+                np.testing.assert_array_equal(sched.seg, seg)
+                np.testing.assert_array_equal(sched.cached, cached)
+                assert (sched.overhead, sched.peak, sched.cache_mem) == (
+                    ref.overhead, ref.peak, ref.cache_mem)
         if table:
             m, a = sol.table()
             rm, ra = ref.table()
@@ -132,17 +134,17 @@ def test_node_limit_antichain(rc, monkeypatch, path):
                 assert sol.status == rc.INFEASIBLE
             else:
                 assert (sol.t_star, sol.m_star) == (TV, 0)
-                sched = sol.reconstruct()
-                assert sched.chain.tolist() == chain
-                assert (sched.overhead, sched.cache_mem) == (TV, 0)
-                assert not sched.cached.any()
-                seg = np.full(n, len(chain) - 1)
-                if len(chain) == 2:
-                    seg[chain[0] - 1] = 0
-                    assert sched.peak == max(2 * big, 2 * (MV - big))
-                else:
-                    assert sched.peak == 2 * MV
-                np.testing.assert_array_equal(sched.seg, seg)
+                for sched in reconstruct_each(sol, n + 2):
+                    assert sched.chain.tolist() == chain
+                    assert (sched.overhead, sched.cache_mem) == (TV, 0)
+                    assert not sched.cached.any()
+                    seg = np.full(n, len(chain) - 1)
+                    if len(chain) == 2:
+                        seg[chain[0] - 1] = 0
+                        assert sched.peak == max(2 * big, 2 * (MV - big))
+                    else:
+                        assert sched.peak == 2 * MV
+                    np.testing.assert_array_equal(sched.seg, seg)
             if objective == "tc":
                 m, a = sol.table()
                 np.testing.assert_array_equal(m, em, err_msg=f"B={B}")
@@ -168,18 +170,18 @@ def test_node_limit_chain(rc, monkeypatch, path):
     B = 2 * n
     sol = fam.solve(B, "tc")
     assert (sol.t_star, sol.m_star) == (1, n - 1)
-    sched = sol.reconstruct()
-    assert sched.chain.tolist() == list(range(1, n + 1))
-    np.testing.assert_array_equal(sched.seg, np.arange(n))
-    assert sched.cached.tolist() == [True] * (n - 1) + [False]
-    assert (sched.overhead, sched.peak, sched.cache_mem) == (1, n + 1, n - 1)
+    for sched in reconstruct_each(sol, n + 1):
+        assert sched.chain.tolist() == list(range(1, n + 1))
+        np.testing.assert_array_equal(sched.seg, np.arange(n))
+        assert sched.cached.tolist() == [True] * (n - 1) + [False]
+        assert (sched.overhead, sched.peak, sched.cache_mem) == (1, n + 1, n - 1)
     m, _ = sol.table(first=n, count=1)
     np.testing.assert_array_equal(m[0], np.array([-1] + [n - t for t in range(1, n + 1)]))
     sol.free()
     sol = fam.solve(B, "mc")
     assert (sol.t_star, sol.m_star) == (n, 0)
-    sched = sol.reconstruct()
-    assert sched.chain.tolist() == [n] and sched.overhead == n and sched.peak == 2 * n
+    for sched in reconstruct_each(sol, n + 1):
+        assert sched.chain.tolist() == [n] and sched.overhead == n and sched.peak == 2 * n
     sol.free()
 
 
