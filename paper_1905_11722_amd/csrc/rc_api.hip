@@ -856,14 +856,14 @@ static int choose_fill_path(rc_family f) {
   if (env && (std::strcmp(env, "wide") == 0 || std::strcmp(env, "ghost") == 0)) return wave;
   if (wave == 1) return 0;
   // The wavefront against the level launches, by their measured costs on
-  // this GPU.  The wavefront runs its 256-cell columns at most three per
-  // compute unit at a time, each through every row of the table at about
-  // 2.5 us per row.  A level launch costs about 6 us, plus the source reads
+  // this GPU.  The wavefront runs its 256-cell columns at most three (the
+  // split-panel fill: four) per compute unit at a time, each through every
+  // row of the table at about 2.5 us per row.  A level launch costs about 6 us, plus the source reads
   // of its pairs (2 bytes per relaxation) at about 4 TB/s.  Few levels of
   // many sets or of very long rows (the ladder and U-Net shapes) take the
   // level launches; many levels take the wavefront.
   const int64_t levels = (int64_t)f->level_ptr.size() - 1;
-  const int64_t slots = 3 * (int64_t)num_cus();
+  const int64_t slots = (wave == 3 ? wide_slots_per_cu(3) : 3) * (int64_t)num_cus();
   const int64_t col_rounds = ((f->max_row + kWC - 1) / kWC + slots - 1) / slots;
   const double wave_us = 2.5 * (double)f->F * (double)col_rounds;
   const double level_us = 6.0 * (double)levels + 2.0 * (double)f->relax / 4.0e6;

@@ -454,6 +454,9 @@ struct WParams {
   DevStatus* st;
   int64_t timeout_ticks;
 };
+// Resident workgroups per compute unit of the split-panel fill with np
+// panel waves: sixteen waves, four per SIMD.
+__host__ __device__ constexpr int wide_slots_per_cu(int np) { return 16 / (np + 1); }
 int64_t wide_columns(rc_family f);
 hipError_t launch_wide_count(rc_family f, int64_t* count, hipStream_t s);
 hipError_t launch_fill_wide(rc_solution sol, hipStream_t s);
