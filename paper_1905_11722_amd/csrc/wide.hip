@@ -264,10 +264,19 @@ __device__ __forceinline__ bool load_row_cells(const WParams& p, __amdgpu_buffer
   }
 }
 
-__device__ __forceinline__ void push_pair(RowLds& L, int q, int k, u16x2 x, u16x2 tau, u16x2 dm) {
+// Relax slot pair q (accumulators of the block or of the next one) with the
+// source cells x[k] of the lane's four cells: the four accumulators are read
+// before any is written, so that the pair waits for LDS once.
+__device__ __forceinline__ void push_pair4(RowLds& L, int q, const u16x2 (&x)[4], u16x2 tau,
+                                           u16x2 dm) {
   const int lane = threadIdx.x & (kWave - 1);
-  uint32_t* a = q < kJB / 2 ? &L.acc[q][lane + 64 * k] : &L.nxt[q - kJB / 2][lane + 64 * k];
-  *a = __builtin_bit_cast(uint32_t, relax2(__builtin_bit_cast(u16x2, *a), x, tau, dm));
+  uint32_t* a = q < kJB / 2 ? &L.acc[q][lane] : &L.nxt[q - kJB / 2][lane];
+  uint32_t v[4];
+#pragma unroll
+  for (int k = 0; k < 4; k++) v[k] = a[64 * k];
+#pragma unroll
+  for (int k = 0; k < 4; k++)
+    a[64 * k] = __builtin_bit_cast(uint32_t, relax2(__builtin_bit_cast(u16x2, v[k]), x[k], tau, dm));
 }
 
 // Row s of block b (push list pdv): store it, then push it into the later
@@ -318,14 +327,21 @@ __device__ __forceinline__ bool row_step(const WParams& p, int32_t c, int s, int
     near_pairs &= near_pairs - 1;
     const int32_t e0 = lane_word(pdv, kWpE + 2 * q), e1 = lane_word(pdv, kWpE + 2 * q + 1);
     const bool n0 = e0 >= 0 && e0 <= kWH, n1 = e1 >= 0 && e1 <= kWH;
+    const int32_t o0 = n0 ? e0 : 0, o1 = n1 ? e1 : 0;     // every read in range, used or not
     const u16x2 tau = as_u16x2(lane_word(pdv, kWpTau + q)), dm = as_u16x2(lane_word(pdv, kWpDm + q));
+    uint16_t r0[4], r1[4];
 #pragma unroll
     for (int k = 0; k < 4; k++) {
-      u16x2 x;
-      x.x = n0 ? L.row[lane + 64 * k + e0] : (uint16_t)kInfM;
-      x.y = n1 ? L.row[lane + 64 * k + e1] : (uint16_t)kInfM;
-      push_pair(L, q, k, x, tau, dm);
+      r0[k] = L.row[lane + 64 * k + o0];
+      r1[k] = L.row[lane + 64 * k + o1];
     }
+    u16x2 x[4];
+#pragma unroll
+    for (int k = 0; k < 4; k++) {
+      x[k].x = n0 ? r0[k] : (uint16_t)kInfM;
+      x[k].y = n1 ? r1[k] : (uint16_t)kInfM;
+    }
+    push_pair4(L, q, x, tau, dm);
   }
   // far pushes (shift beyond the halo): the source cells straight from the table
   uint32_t fm = far;
@@ -337,13 +353,13 @@ __device__ __forceinline__ bool row_step(const WParams& p, int32_t c, int s, int
     if (!load_row_cells<4>(p, rm, endj, Pj, u0 + e, 4, f)) return false;
     const int q = t >> 1;
     const u16x2 tau = as_u16x2(lane_word(pdv, kWpTau + q)), dm = as_u16x2(lane_word(pdv, kWpDm + q));
+    u16x2 x[4];
 #pragma unroll
     for (int k = 0; k < 4; k++) {
-      u16x2 x;
-      x.x = (t & 1) ? (uint16_t)kInfM : (uint16_t)f[k];
-      x.y = (t & 1) ? (uint16_t)f[k] : (uint16_t)kInfM;
-      push_pair(L, q, k, x, tau, dm);
+      x[k].x = (t & 1) ? (uint16_t)kInfM : (uint16_t)f[k];
+      x[k].y = (t & 1) ? (uint16_t)f[k] : (uint16_t)kInfM;
     }
+    push_pair4(L, q, x, tau, dm);
   }
   return true;
 }
