@@ -381,8 +381,9 @@ static int32_t family_block_kind(rc_family f, bool shape_known) {
   // fixed blocks, so that the split-panel fill can take the family, for
   // rows of 2^16 cells and more and for families of kWideMinSets sets and
   // more (measured faster than the ghost-zone fill on every such shape
-  // here: the ghost blocks hold fewer rows, so that each staged window
-  // serves fewer targets); ghost-zone blocks for the smaller families
+  // here, resnet50_t10's 175 sets included: the ghost blocks hold fewer
+  // rows, so that each staged window serves fewer targets); ghost-zone
+  // blocks for the smaller families
   return f->max_row >= 65536 || F >= kWideMinSets ? kBlocksFixed : kBlocksGhost;
 }
 

@@ -40,7 +40,7 @@ constexpr int kBlocksFixed = 1;                 // family blocks: kJB targets ea
 constexpr int kBlocksGhost = 2;                 // family blocks: cut to fit the ghost halo
 constexpr int kGhostHalo = 64;                  // ghost-zone fill: cells recomputed to the right
 constexpr int kGhostMaxSets = 4096;             // ghost-zone fill: largest family it takes
-constexpr int kWideMinSets = 200;               // families this large take the split-panel fill
+constexpr int kWideMinSets = 100;               // families this large take the split-panel fill
 constexpr int kNear = kJB;                      // ghost cut: predecessors j-1 .. j-kNear examined
 constexpr int kTriInts = 16;                    // ghost-zone fill: int32 per (block, row) list
 constexpr int kWC = 256;                        // split-panel fill: cells per column
