@@ -279,6 +279,57 @@ __device__ __forceinline__ void push_pair4(RowLds& L, int q, const u16x2 (&x)[4]
     a[64 * k] = __builtin_bit_cast(uint32_t, relax2(__builtin_bit_cast(u16x2, v[k]), x[k], tau, dm));
 }
 
+// Issues the loads of the row's cells at u = ubase + lane + 64 k (k < 4);
+// cells outside the row read the trailing guard's infinity.
+__device__ __forceinline__ void far_loads(const WParams& p, __amdgpu_buffer_rsrc_t rm, int64_t endj,
+                                          int32_t Pj, int32_t ubase, int32_t (&off)[4],
+                                          uint32_t (&out)[4]) {
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int k = 0; k < 4; k++) {
+    const int32_t u = ubase + lane + 64 * k;
+    off[k] = (u <= 0 && u >= -Pj) ? (int32_t)(2 * (endj + u)) : p.null_off;
+    out[k] = ld_cell(rm, off[k], 0);
+  }
+}
+
+// Repeats the loads at byte offsets off[] that returned kPendM (not written
+// yet) until none does; false on timeout.
+template <int N>
+__device__ __forceinline__ bool poll_cells(const WParams& p, __amdgpu_buffer_rsrc_t rm,
+                                           const int32_t (&off)[N], uint32_t (&out)[N]) {
+  bool pend = false;
+#pragma unroll
+  for (int k = 0; k < N; k++) pend |= out[k] == kPendM;
+  if (!__any(pend)) return true;
+  const long long t0 = wall_clock64();
+  while (true) {
+    __builtin_amdgcn_s_sleep(1);
+    pend = false;
+#pragma unroll
+    for (int k = 0; k < N; k++)
+      if (out[k] == kPendM) {
+        out[k] = ld_cell(rm, off[k], 0);
+        pend |= out[k] == kPendM;
+      }
+    if (!__any(pend)) return true;
+    if (wall_clock64() - t0 > p.timeout_ticks) return false;
+  }
+}
+
+// The far push of slot t (one slot of pair t / 2) with source cells f.
+__device__ __forceinline__ void far_push(RowLds& L, int32_t pdv, int t, const uint32_t (&f)[4]) {
+  const int q = t >> 1;
+  const u16x2 tau = as_u16x2(lane_word(pdv, kWpTau + q)), dm = as_u16x2(lane_word(pdv, kWpDm + q));
+  u16x2 x[4];
+#pragma unroll
+  for (int k = 0; k < 4; k++) {
+    x[k].x = (t & 1) ? (uint16_t)kInfM : (uint16_t)f[k];
+    x[k].y = (t & 1) ? (uint16_t)f[k] : (uint16_t)kInfM;
+  }
+  push_pair4(L, q, x, tau, dm);
+}
+
 // Row s of block b (push list pdv): store it, then push it into the later
 // rows of the block (L.acc) and the rows of the next block (L.nxt).  False on
 // timeout.
@@ -343,23 +394,23 @@ __device__ __forceinline__ bool row_step(const WParams& p, int32_t c, int s, int
     }
     push_pair4(L, q, x, tau, dm);
   }
-  // far pushes (shift beyond the halo): the source cells straight from the table
+  // far pushes (shift beyond the halo): the source cells straight from the
+  // table, two slots at a time, both slots' loads in flight together (with
+  // one slot left, the second is the same slot again: its push repeats the
+  // first's values)
   uint32_t fm = far;
   while (fm) {
-    const int t = __builtin_ctz(fm);
+    const int ta = __builtin_ctz(fm);
     fm &= fm - 1;
-    const int32_t e = lane_word(pdv, kWpE + t);
-    uint32_t f[4];
-    if (!load_row_cells<4>(p, rm, endj, Pj, u0 + e, 4, f)) return false;
-    const int q = t >> 1;
-    const u16x2 tau = as_u16x2(lane_word(pdv, kWpTau + q)), dm = as_u16x2(lane_word(pdv, kWpDm + q));
-    u16x2 x[4];
-#pragma unroll
-    for (int k = 0; k < 4; k++) {
-      x[k].x = (t & 1) ? (uint16_t)kInfM : (uint16_t)f[k];
-      x[k].y = (t & 1) ? (uint16_t)f[k] : (uint16_t)kInfM;
-    }
-    push_pair4(L, q, x, tau, dm);
+    const int tb = fm ? __builtin_ctz(fm) : ta;
+    fm &= fm - 1;
+    int32_t oa[4], ob[4];
+    uint32_t fa[4], fb[4];
+    far_loads(p, rm, endj, Pj, u0 + lane_word(pdv, kWpE + ta), oa, fa);
+    far_loads(p, rm, endj, Pj, u0 + lane_word(pdv, kWpE + tb), ob, fb);
+    if (!poll_cells<4>(p, rm, oa, fa) || !poll_cells<4>(p, rm, ob, fb)) return false;
+    far_push(L, pdv, ta, fa);
+    far_push(L, pdv, tb, fb);
   }
   return true;
 }
