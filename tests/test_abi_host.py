@@ -68,6 +68,9 @@ def test_null_handles():
     assert lib.rc_reconstruct(None, None, None, None, None, None, None, None, None) == rcdp.E_ARG
     assert lib.rc_export_table(None, 0, 0, None, None, None) == rcdp.E_ARG
     assert lib.rc_family_sets(None, None, None) == rcdp.E_ARG
+    path = ctypes.c_int32()
+    assert lib.rc_solution_fill_path(None, ctypes.byref(path)) == rcdp.E_ARG
+    assert lib.rc_solution_trace_path(None, ctypes.byref(path)) == rcdp.E_ARG
     lib.rc_graph_free(None)
     lib.rc_family_free(None)
     lib.rc_solution_free(None)

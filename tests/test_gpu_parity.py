@@ -359,6 +359,26 @@ def test_fill_path_is_reported(rc, monkeypatch, path, kernel):
     sol.free()
 
 
+@pytest.mark.parametrize("name,objective,kernel", [("densenet121", "tc", "k_trace_follow"),
+                                                    ("resnet50_t10", "tc", "k_trace_follow"),
+                                                    ("ladder40", "mc", "k_trace"),
+                                                    ("unet", "mc", "k_trace")])
+def test_trace_path_choice(rc, monkeypatch, name, objective, kernel):
+    """The default traceback: the optarg slice where t* is small and the
+    chain may be long, the predecessor scan where the slice's tests would
+    cost more than the longest chain (the memory-centric optima, t* large);
+    the schedule meets t*, opt[V, t*] and the budget either way."""
+    monkeypatch.delenv("RCDP_TRACE", raising=False)
+    c = W.case(name)
+    fam = rc.Graph.create(c.graph).build_family(c.mode)
+    sol = fam.solve(c.B, objective)
+    assert sol.trace_kernel() is None
+    sched = sol.reconstruct()
+    assert sol.trace_kernel() == kernel
+    assert (sched.overhead, sched.cache_mem) == (sol.t_star, sol.m_star) and sched.peak <= c.B
+    sol.free()
+
+
 @pytest.mark.parametrize("n,p,seed", WIDE[::2])
 def test_wide_fill_four_panel_waves(rc, oracle_mod, monkeypatch, n, p, seed):
     """The split-panel fill with four panel waves per workgroup."""
