@@ -648,9 +648,9 @@ __global__ __launch_bounds__(kArgWaves* kWave) void k_trace_args(
 }
 
 // The walk over the slice of k_trace_args from (V, t*), then Eq. 1 and
-// Eq. 2 of the chain as in k_trace.  Thread 0 walks; the other waves first
-// read the slice from its last row down (the order of the walk), so that
-// the walk's loads find it in this compute unit's L2.
+// Eq. 2 of the chain as in k_trace.  Thread 0 walks; meanwhile the other
+// waves read the slice from its last row down (the order of the walk), so
+// that most of the walk's loads hit the L2 of the XCD it runs on.
 __global__ __launch_bounds__(kTraceThreads) void k_trace_follow(
     int64_t F, int n, int words, int64_t fstride, const uint64_t* __restrict__ bits,
     const uint64_t* __restrict__ bd, const int32_t* __restrict__ A, const int32_t* __restrict__ T,
