@@ -379,6 +379,44 @@ def test_trace_path_choice(rc, monkeypatch, name, objective, kernel):
     sol.free()
 
 
+def test_random_tracebacks(rc, oracle_mod):
+    """Both tracebacks against the oracle's schedule on 300 seeded random
+    DAGs (2-13 nodes, edge densities 0.1-0.85, small and large costs), a
+    random budget around the feasible range, both families and objectives."""
+    import random
+    from tests.trace_paths import forced_trace, expected_kernel
+    rng = random.Random(20261202)
+    checked = 0
+    for it in range(300):
+        n = rng.randint(2, 13)
+        p = rng.choice([0.1, 0.25, 0.4, 0.6, 0.85])
+        g = W.random_dag(n, p, rng.randint(0, 10 ** 6), tmax=rng.choice([5, 40, 300]),
+                         mmax=rng.choice([3, 30, 200]))
+        lo, hi = 2 * max(g.M), 2 * sum(g.M)
+        B = rng.randint(max(0, lo - 5), hi + 5)
+        mode = rng.choice(["exact", "pruned"])
+        fam = rc.Graph.create(g).build_family(mode)
+        for objective in ("tc", "mc"):
+            ref = oracle_mod.solve(g, mode, B, objective)
+            sol = fam.solve(B, objective)
+            assert (sol.t_star, sol.m_star) == (ref.t_star, ref.m_star), (it, B, mode, objective)
+            if ref.status == oracle_mod.OK:
+                chain, seg, cached = ref.schedule()
+                for trace in ("scan", "slice"):
+                    with forced_trace(trace):
+                        sched = sol.reconstruct()
+                    assert sol.trace_kernel() == expected_kernel(trace, ref.num_sets, sol.t_star)
+                    np.testing.assert_array_equal(sched.chain, chain, err_msg=f"{it} {trace}")
+                    np.testing.assert_array_equal(sched.seg, seg)
+                    np.testing.assert_array_equal(sched.cached, cached)
+                    assert (sched.overhead, sched.peak, sched.cache_mem) == (
+                        ref.overhead, ref.peak, ref.cache_mem)
+                    checked += 1
+            sol.free()
+        fam.free()
+    assert checked > 400
+
+
 @pytest.mark.parametrize("n,p,seed", WIDE[::2])
 def test_wide_fill_four_panel_waves(rc, oracle_mod, monkeypatch, n, p, seed):
     """The split-panel fill with four panel waves per workgroup."""
