@@ -788,9 +788,16 @@ int64_t wait_ticks() {
   return (int64_t)clock_khz * 1000 * 4;                // 4 s per wait
 }
 
-int wide_panel_waves() {
+// Panel waves per workgroup for a launch of `cols` columns (all tables).
+// Three, unless the launch holds more than two rounds of the resident
+// columns (a batched sweep): then two, so that five workgroups fit per
+// compute unit instead of four and more row chains run side by side
+// (config 3's 32-budget sweep: 9.3 ms against 10.6; a single table's fill
+// is as fast or slower with two).
+int wide_panel_waves(int64_t cols) {
   const char* env = std::getenv("RCDP_WIDE_NP");
-  return env && env[0] == '4' ? 4 : 3;
+  if (env && (env[0] == '2' || env[0] == '3' || env[0] == '4')) return env[0] - '0';
+  return cols > 2 * (int64_t)wide_slots_per_cu(3) * num_cus() ? 2 : 3;
 }
 
 }  // namespace
@@ -846,8 +853,8 @@ static hipError_t prepare_wide(rc_solution sol, int32_t K, int32_t* ticket, WPar
 
 static hipError_t launch_wide_kernel(const WParams& prm, const WParams* dev, int32_t nb,
                                      hipEvent_t e0, hipEvent_t e1, hipStream_t s) {
-  const int np = wide_panel_waves();
   const int64_t cols = (int64_t)prm.K * nb;
+  const int np = wide_panel_waves(cols);
   const int32_t grid = (int32_t)std::min<int64_t>(cols, (int64_t)num_cus() * wide_slots_per_cu(np));
   if (std::getenv("RCDP_DEBUG"))
     std::fprintf(stderr, "rcdp: split-panel fill %d table(s) x K=%d columns of %d cells, "
@@ -855,6 +862,8 @@ static hipError_t launch_wide_kernel(const WParams& prm, const WParams* dev, int
   if (e0 && hipEventRecord(e0, s) != hipSuccess) return hipErrorUnknown;
   if (np == 4)
     hipLaunchKernelGGL(k_fill_wide<4>, dim3(grid), dim3(5 * kWave), 0, s, prm, dev, nb);
+  else if (np == 2)
+    hipLaunchKernelGGL(k_fill_wide<2>, dim3(grid), dim3(3 * kWave), 0, s, prm, dev, nb);
   else
     hipLaunchKernelGGL(k_fill_wide<3>, dim3(grid), dim3(4 * kWave), 0, s, prm, dev, nb);
   const hipError_t e = hipGetLastError();
