@@ -50,9 +50,9 @@
  *    (k_fill_ghost; families of at most 4096 sets).  Unset: chosen from the
  *    family's size, width and number of levels (rc_solution_fill_path
  *    reports the choice).
- *  - RCDP_WIDE_NP = 2 | 3 | 4: panel waves per workgroup of k_fill_wide
- *    (default 3, or 2 for a batched launch of more than twice the columns
- *    that fit on the GPU at once).
+ *  - RCDP_WIDE_NP = 1 | 2 | 3 | 4: panel waves per workgroup of
+ *    k_fill_wide (default 3, or 1 for a launch of more columns than fit on
+ *    the GPU at once with three: batched sweeps and the widest tables).
  *  - RCDP_CPT = 1 | 2 | 4: cells per thread of a k_fill_blocked column
  *    (default from the table's width).
  *  - RCDP_GHOST_CPT = 1 | 2: cells per thread of a k_fill_ghost column

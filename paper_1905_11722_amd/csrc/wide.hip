@@ -789,15 +789,17 @@ int64_t wait_ticks() {
 }
 
 // Panel waves per workgroup for a launch of `cols` columns (all tables).
-// Three, unless the launch holds more than two rounds of the resident
-// columns (a batched sweep): then two, so that five workgroups fit per
-// compute unit instead of four and more row chains run side by side
-// (config 3's 32-budget sweep: 9.3 ms against 10.6; a single table's fill
-// is as fast or slower with two).
+// Three while every column fits on the GPU at once with four workgroups per
+// compute unit; beyond that one, so that eight workgroups fit per compute
+// unit and twice as many row chains run side by side, each column's panel
+// on one wave (config 3's 32-budget sweep: fill 7.4 ms against 9.3 with
+// two panel waves and 10.6 with three; config 3's single table, 1031
+// columns: 0.61 ms against 0.63; config 4, 720 columns, keeps three:
+// 1.74 ms against 2.30 with one).
 int wide_panel_waves(int64_t cols) {
   const char* env = std::getenv("RCDP_WIDE_NP");
-  if (env && (env[0] == '2' || env[0] == '3' || env[0] == '4')) return env[0] - '0';
-  return cols > 2 * (int64_t)wide_slots_per_cu(3) * num_cus() ? 2 : 3;
+  if (env && env[0] >= '1' && env[0] <= '4') return env[0] - '0';
+  return cols > (int64_t)wide_slots_per_cu(3) * num_cus() ? 1 : 3;
 }
 
 }  // namespace
@@ -864,6 +866,8 @@ static hipError_t launch_wide_kernel(const WParams& prm, const WParams* dev, int
     hipLaunchKernelGGL(k_fill_wide<4>, dim3(grid), dim3(5 * kWave), 0, s, prm, dev, nb);
   else if (np == 2)
     hipLaunchKernelGGL(k_fill_wide<2>, dim3(grid), dim3(3 * kWave), 0, s, prm, dev, nb);
+  else if (np == 1)
+    hipLaunchKernelGGL(k_fill_wide<1>, dim3(grid), dim3(2 * kWave), 0, s, prm, dev, nb);
   else
     hipLaunchKernelGGL(k_fill_wide<3>, dim3(grid), dim3(4 * kWave), 0, s, prm, dev, nb);
   const hipError_t e = hipGetLastError();

@@ -417,11 +417,11 @@ def test_random_tracebacks(rc, oracle_mod):
     assert checked > 400
 
 
-@pytest.mark.parametrize("np_", ["2", "4"])
+@pytest.mark.parametrize("np_", ["1", "2", "4"])
 @pytest.mark.parametrize("n,p,seed", WIDE[::2])
 def test_wide_fill_panel_waves(rc, oracle_mod, monkeypatch, np_, n, p, seed):
-    """The split-panel fill with two (the batched sweeps' choice) and four
-    panel waves per workgroup."""
+    """The split-panel fill with one (the choice for launches of more
+    columns than fit at once), two and four panel waves per workgroup."""
     monkeypatch.setenv("RCDP_FILL", "wide")
     monkeypatch.setenv("RCDP_WIDE_NP", np_)
     g = W.random_dag(n, p, 8000 + seed, tmax=900, mmax=60)
@@ -614,15 +614,15 @@ def test_paper_cost_convention(rc, oracle_mod, name):
     compare(rc, oracle_mod, c.graph, c.mode, fam.min_budget())
 
 
-@pytest.mark.parametrize("path", PATHS + ["wide2"])
+@pytest.mark.parametrize("path", PATHS + ["wide1"])
 @pytest.mark.parametrize("n,p,seed", WIDE[2::5])
 def test_solve_batch_tables(rc, oracle_mod, monkeypatch, path, n, p, seed):
     """rc_solve_batch: every budget's table, t* and schedule as the oracle's,
-    the tables of all budgets filled in one pass ("wide2": the split-panel
-    fill with two panel waves, the batched sweeps' choice)."""
-    monkeypatch.setenv("RCDP_FILL", "wide" if path == "wide2" else path)
-    if path == "wide2":
-        monkeypatch.setenv("RCDP_WIDE_NP", "2")
+    the tables of all budgets filled in one pass ("wide1": the split-panel
+    fill with one panel wave, the choice for large batched sweeps)."""
+    monkeypatch.setenv("RCDP_FILL", "wide" if path == "wide1" else path)
+    if path == "wide1":
+        monkeypatch.setenv("RCDP_WIDE_NP", "1")
     g = W.random_dag(n, p, 5000 + seed, tmax=700, mmax=60)
     lo, hi = 2 * max(g.M), 2 * sum(g.M)
     budgets = [lo, (3 * lo + hi) // 4, (lo + hi) // 2, hi, lo - 1]
